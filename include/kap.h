@@ -1,0 +1,221 @@
+/*
+ * kap.h -- C ABI of the KAP selected-KV decode / full-KV verify library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "KAP: Bridging the Knowledge Selection--Runtime Consumption Gap in
+ * LLM Systems" (arXiv 2607.24260). The library implements the data-parallel
+ * part of the GraphSpec executor:
+ *
+ *   kap_compile_plan     Alg. 1 (GraphSpecCompile): select evidence spans
+ *                        under a token budget by prior score, resolve them to
+ *                        KV pages, keep their logical positions and build the
+ *                        proposal-side block table (Sec. 3.1).
+ *   kap_selected_decode  one proposal step, q_prop = 1, whose attention reads
+ *                        only the KV pages the plan exposes (Sec. 3.2,
+ *                        "Selected-KV proposal").
+ *   kap_verify           causal attention of the k+1 verify window over the
+ *                        full paged KV cache (Sec. 3.2, "Full-context
+ *                        verification"; Eq. (2)).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every array argument is device memory owned by the caller. The library
+ *   never allocates, frees or synchronises, and keeps no pointer after the
+ *   call returns. Work is enqueued on `stream` (a hipStream_t passed as
+ *   void*; NULL = the default stream); the caller keeps every buffer alive
+ *   until that work has completed.
+ * - Scratch memory comes from the caller's `workspace`, at least the size the
+ *   matching kap_*_workspace_bytes() call returns for the same arguments on
+ *   the current device. Its contents on entry do not matter.
+ * - Grid sizes depend only on host integers, never on device data, so the
+ *   calls may be captured into a HIP graph.
+ * - Host-checkable errors (null pointers, negative sizes, unsupported
+ *   geometry or dtype, small workspace) return a non-zero kap_status before
+ *   anything is enqueued. batch == 0 is a successful no-op. A failed launch
+ *   returns KAP_ERR_HIP. kap_last_error() then describes the problem.
+ * - Data-dependent problems of kap_compile_plan are reported per sequence in
+ *   plan_status[] (KAP_PLAN_*); the call itself returns KAP_OK.
+ * - kap_selected_decode and kap_verify never dereference a page id outside
+ *   [0, num_pages): such a page contributes no keys. Results for such inputs
+ *   are otherwise unspecified.
+ *
+ * KV cache layout (struct kap_kv_cache)
+ * -------------------------------------
+ *   k_pages: [num_pages][num_kv_heads][page_size][head_dim]  token-major pages
+ *   v_pages: [num_pages][num_kv_heads][head_dim][page_size]  dim-major pages
+ *   kv_scales (FP8 only): [num_pages][2] float, K scale then V scale; a stored
+ *            E4M3FN code x of page p stands for decode(x) * scale.
+ * Token t of logical page j of a sequence is its token 16*j + t; logical page j
+ * lives in physical page block_table[j]. Query head h reads KV head
+ * h / (num_q_heads / num_kv_heads).
+ * Supported: page_size 16; head_dim 128 (64 and 256 on the generic path);
+ * num_q_heads a multiple of num_kv_heads; kv_dtype F32 with q_dtype F32, or
+ * kv_dtype BF16 / FP8_E4M3FN with q_dtype BF16.
+ *
+ * Outputs of attention are float32: out = softmax(z) V and lse = natural
+ * log-sum-exp of z, with z = sm_scale * <q, k>. A row that sees no key gets
+ * out = 0 and lse = -inf.
+ */
+#ifndef KAP_H_
+#define KAP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KAP_ABI_VERSION 1
+
+typedef int32_t kap_status;
+enum {
+  KAP_OK = 0,
+  KAP_ERR_INVALID_ARGUMENT = 1,
+  KAP_ERR_UNSUPPORTED = 2,
+  KAP_ERR_WORKSPACE_TOO_SMALL = 3,
+  KAP_ERR_HIP = 4
+};
+
+typedef int32_t kap_dtype;
+enum { KAP_DT_F32 = 0, KAP_DT_BF16 = 1, KAP_DT_FP8_E4M3FN = 2 };
+
+/* What kap_compile_plan does with a span that does not fit the budget. */
+typedef int32_t kap_select_policy;
+enum { KAP_SELECT_SKIP = 0, KAP_SELECT_STOP = 1 };
+
+/* Per-sequence plan status (fallback triggers, Sec. 3.2 "Runtime stability
+ * and fallback"). Any value other than KAP_PLAN_OK means: the sequence's view
+ * is empty (view_num_blocks = view_tokens = spans_taken = 0, its span_selected
+ * flags are 0) and the executor must use full-context access. */
+enum {
+  KAP_PLAN_OK = 0,
+  KAP_PLAN_OVER_CAPACITY = 1, /* the view needs more than view_capacity blocks */
+  KAP_PLAN_BAD_SCORE = 2,     /* a prior score is NaN */
+  KAP_PLAN_BAD_PAGE = 3,      /* a selected page id is outside [0, num_pages) */
+  KAP_PLAN_BAD_LENGTH = 4,    /* seq_len < 1 or ceil(seq_len/16) > fbt_stride */
+  KAP_PLAN_BAD_SPANS = 5      /* span_offsets[b..b+1] not within [0, num_spans] */
+};
+
+typedef struct kap_kv_cache {
+  int32_t num_q_heads;  /* Hq */
+  int32_t num_kv_heads; /* Hkv; Hq % Hkv == 0 */
+  int32_t head_dim;     /* D */
+  int32_t page_size;    /* tokens per page: 16 */
+  kap_dtype kv_dtype;
+  kap_dtype q_dtype;
+  const void *k_pages;
+  const void *v_pages;
+  const float *kv_scales; /* FP8 only, else NULL */
+  int64_t num_pages;
+} kap_kv_cache;
+
+/*
+ * kap_compile_plan -- Alg. 1, SelectEvidenceUnderBudget through
+ * EmitRuntimeAccessPlan, for `batch` sequences at once.
+ *
+ * Per sequence b (L = seq_lens[b], NP = ceil(L/16), valid(j) = min(16, L-16j)):
+ *  1. Mandatory pages: those touched by tokens [0, min(prefix,L)) and by
+ *     [max(0, L - max(suffix,1)), L); the page of the last token is always in.
+ *     used = sum of valid(j) over the selected pages.
+ *  2. Spans i in [span_offsets[b], span_offsets[b+1]) are clipped to [0, L)
+ *     and ranked by (span_prior desc, span_start asc, i asc); -0 == +0.
+ *  3. In rank order, a non-empty span whose not-yet-selected pages cost
+ *     `cost` visible tokens is taken iff used + cost <= budget_tokens[b]
+ *     (then used += cost). A span that does not fit is skipped
+ *     (KAP_SELECT_SKIP) or ends selection (KAP_SELECT_STOP). Empty spans are
+ *     ignored.
+ *  4. view_logical_block[b][0..n) = selected logical pages ascending,
+ *     view_block_table[b][k] = full_block_table[b][view_logical_block[b][k]],
+ *     view_num_blocks[b] = n, view_tokens[b] = used (the numerator of the
+ *     retained ratio s, Eq. (4)), spans_taken[b] = number of spans taken,
+ *     span_selected[i] = 1 for taken spans else 0 (may be NULL).
+ *
+ * Arguments (device arrays unless noted):
+ *   seq_lens [batch] int32; full_block_table [batch][fbt_stride] int32;
+ *   span_offsets [batch+1] int32 (CSR); num_spans (host) = length of the span
+ *   arrays; span_start, span_len [num_spans] int32; span_prior [num_spans]
+ *   float32; prefix_tokens, suffix_tokens, budget_tokens [batch] int32;
+ *   policy (host); num_pages (host) bounds valid page ids; view_capacity
+ *   (host) = row stride of the view arrays and the most blocks a view may
+ *   have; outputs view_block_table, view_logical_block [batch][view_capacity]
+ *   int32 (entries past view_num_blocks[b] are left unchanged),
+ *   view_num_blocks, view_tokens, spans_taken, plan_status [batch] int32,
+ *   span_selected [num_spans] int32 or NULL.
+ * Limits: fbt_stride <= 262144 pages per sequence.
+ * Result is unique and bit-for-bit deterministic.
+ */
+kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens,
+                            const int32_t *full_block_table, int32_t fbt_stride,
+                            const int32_t *span_offsets, int32_t num_spans,
+                            const int32_t *span_start, const int32_t *span_len,
+                            const float *span_prior, const int32_t *prefix_tokens,
+                            const int32_t *suffix_tokens, const int32_t *budget_tokens,
+                            kap_select_policy policy, int64_t num_pages,
+                            int32_t view_capacity, int32_t *view_block_table,
+                            int32_t *view_logical_block, int32_t *view_num_blocks,
+                            int32_t *view_tokens, int32_t *spans_taken,
+                            int32_t *plan_status, int32_t *span_selected,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+size_t kap_compile_plan_workspace_bytes(int32_t batch, int32_t num_spans,
+                                        int32_t fbt_stride);
+
+/*
+ * kap_selected_decode -- one proposal step (q_prop = 1) over the selected-KV
+ * view (Sec. 3.2, "Selected-KV proposal").
+ *
+ * For sequence b and query head h, the visible keys are, for each
+ * k < min(view_num_blocks[b], max_view_blocks), the tokens t < min(16,
+ * seq_lens[b] - 16*view_logical_block[b][k]) of physical page
+ * view_block_table[b][k]. The order of view blocks does not change the result.
+ *   q [batch][Hq][D] (q_dtype); view arrays [batch][view_stride] int32 with
+ *   view_stride >= max_view_blocks; view_num_blocks, seq_lens [batch] int32;
+ *   out [batch][Hq][D] float32; lse [batch][Hq] float32.
+ * num_splits (host): 0 = automatic; n > 0 forces n key splits per
+ * (sequence, KV head) (clamped to the number of view blocks).
+ * Passing the full block table as the view, with view_logical_block[b][j] = j
+ * and view_num_blocks[b] = ceil(seq_lens[b]/16), is full-context decode.
+ */
+kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void *q,
+                               const int32_t *seq_lens, const int32_t *view_block_table,
+                               const int32_t *view_logical_block, int32_t view_stride,
+                               const int32_t *view_num_blocks, int32_t max_view_blocks,
+                               float sm_scale, int32_t num_splits, float *out, float *lse,
+                               void *workspace, size_t workspace_bytes, void *stream);
+
+size_t kap_selected_decode_workspace_bytes(const kap_kv_cache *kv, int32_t batch,
+                                           int32_t max_view_blocks, int32_t num_splits);
+
+/*
+ * kap_verify -- full-context verification attention of the q_len = k+1
+ * window (Sec. 3.2, "Full-context verification"; Eq. (2)).
+ *
+ * The window's own K/V are the last q_len tokens already in the cache, so
+ * seq_lens[b] counts them. Window row i of sequence b sees logical positions
+ * 0 .. seq_lens[b] - q_len + i, read through full_block_table[b].
+ *   q [batch][q_len][Hq][D] (q_dtype); full_block_table [batch][fbt_stride];
+ *   max_seq_len (host) >= every seq_lens[b] and <= 16 * fbt_stride;
+ *   out [batch][q_len][Hq][D] float32; lse [batch][q_len][Hq] float32.
+ * 1 <= q_len <= 16. num_splits as for kap_selected_decode.
+ */
+kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, const void *q,
+                      const int32_t *seq_lens, const int32_t *full_block_table,
+                      int32_t fbt_stride, int32_t max_seq_len, float sm_scale,
+                      int32_t num_splits, float *out, float *lse, void *workspace,
+                      size_t workspace_bytes, void *stream);
+
+size_t kap_verify_workspace_bytes(const kap_kv_cache *kv, int32_t batch, int32_t q_len,
+                                  int32_t max_seq_len, int32_t num_splits);
+
+/* Static description of a status code. */
+const char *kap_status_string(kap_status status);
+/* Message of the last failing call on this thread ("" if none). */
+const char *kap_last_error(void);
+/* KAP_ABI_VERSION of the loaded library. */
+int32_t kap_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KAP_H_ */

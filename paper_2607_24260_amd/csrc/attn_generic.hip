@@ -1,0 +1,145 @@
+// Generic split-KV attention for any KV dtype, any GQA ratio and head_dim in
+// {64, 128, 256}: one wavefront per (sequence, query row, key split).
+//
+// It serves the float32 workload and geometries the tuned kernels do not
+// cover. Each work item stages up to 1024 scores in LDS: pass 1 (lanes over
+// keys) computes the scaled logits, pass 2 (lanes over head dims) forms the
+// normalised partial output. Partials go to the workspace; the LSE merge kernel
+// (merge.hip) combines the splits.
+#include "kap_internal.h"
+
+namespace kap {
+namespace {
+
+template <int KV>
+__device__ __forceinline__ float load_elem(const void *base, size_t idx) {
+  if constexpr (KV == kF32) {
+    return static_cast<const float *>(base)[idx];
+  } else if constexpr (KV == kBF16) {
+    const uint16_t h = static_cast<const uint16_t *>(base)[idx];
+    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+  } else {
+    return fp8_to_f32(static_cast<const uint8_t *>(base)[idx]);
+  }
+}
+
+template <int KV, int D>
+__global__ __launch_bounds__(64) void attn_generic_kernel(AttnArgs a) {
+  constexpr int kKeys = kGenericPagesPerSplit * kPage;
+  __shared__ float qs[D];
+  __shared__ float ps[kKeys];
+
+  const int split = blockIdx.x;
+  const int r = blockIdx.y;          // row within the sequence
+  const int b = blockIdx.z;
+  const int lane = threadIdx.x;
+  const int R = a.q_len * a.Hq;
+  const int i = r / a.Hq;
+  const int h = r % a.Hq;
+  const int g = h / a.G;
+
+  const int L = a.seq_lens[b];
+  const int np_seq = L > 0 ? (int)(((long long)L + kPage - 1) / kPage) : 0;
+  int nb = a.num_blocks ? a.num_blocks[b] : np_seq;
+  nb = max(0, min(nb, a.max_blocks));
+  const int limit = a.causal ? (L - a.q_len + i + 1) : L;   // visible positions < limit
+  const int k0 = split * a.pages_per_split;
+  const int k1 = min(nb, k0 + a.pages_per_split);
+  const size_t row = (size_t)b * R + r;
+  float *po = (a.n_split == 1) ? a.out + row * D : a.part_o + (row * a.n_split + split) * D;
+
+  // query row -> LDS (float)
+  for (int d = lane; d < D; d += 64) {
+    const size_t qi = row * D + d;
+    qs[d] = a.q_f32 ? static_cast<const float *>(a.q)[qi]
+                    : __uint_as_float(static_cast<uint32_t>(
+                          static_cast<const uint16_t *>(a.q)[qi]) << 16);
+  }
+  __syncthreads();
+
+  // pass 1: scaled logits (log2 units), lanes over keys
+  const int nkeys = max(0, k1 - k0) * kPage;
+  float mx = -INFINITY;
+  for (int t = lane; t < nkeys; t += 64) {
+    const int k = k0 + t / kPage;
+    const int tok = t % kPage;
+    const int page = a.block_table[(size_t)b * a.bt_stride + k];
+    const int lb = a.logical_block ? a.logical_block[(size_t)b * a.bt_stride + k] : k;
+    const long long pos = (long long)lb * kPage + tok;
+    float z = -INFINITY;
+    if (page >= 0 && page < a.num_pages && pos < limit && pos < L) {
+      const size_t kbase = (((size_t)page * a.Hkv + g) * kPage + tok) * D;
+      float acc = 0.f;
+      for (int d = 0; d < D; ++d) acc = fmaf(qs[d], load_elem<KV>(a.k_pages, kbase + d), acc);
+      if constexpr (KV == kFP8) acc *= a.kv_scales[2 * (size_t)page];
+      z = acc * a.scale_log2;
+    }
+    ps[t] = z;
+    mx = fmaxf(mx, z);
+  }
+  mx = wave_max(mx);
+  const size_t lse_idx = (a.n_split == 1) ? row : row * a.n_split + split;
+  if (mx == -INFINITY) {
+    for (int d = lane; d < D; d += 64) po[d] = 0.f;
+    if (lane == 0) {
+      if (a.n_split == 1) a.lse[lse_idx] = -INFINITY;
+      else a.part_lse[lse_idx] = -INFINITY;
+    }
+    return;
+  }
+  float sum = 0.f;
+  for (int t = lane; t < nkeys; t += 64) {
+    const float p = exp2f(ps[t] - mx);
+    ps[t] = p;
+    sum += p;
+  }
+  sum = wave_sum(sum);
+  __syncthreads();
+
+  // pass 2: lanes over head dims
+  for (int d = lane; d < D; d += 64) {
+    float acc = 0.f;
+    for (int t = 0; t < nkeys; ++t) {
+      const float p = ps[t];
+      if (p == 0.f) continue;
+      const int k = k0 + t / kPage;
+      const int tok = t % kPage;
+      const int page = a.block_table[(size_t)b * a.bt_stride + k];
+      const size_t vidx = (((size_t)page * a.Hkv + g) * D + d) * kPage + tok;
+      float v = load_elem<KV>(a.v_pages, vidx);
+      if constexpr (KV == kFP8) v *= a.kv_scales[2 * (size_t)page + 1];
+      acc = fmaf(p, v, acc);
+    }
+    po[d] = acc / sum;
+  }
+  if (lane == 0) {
+    const float l2 = mx + log2f(sum);
+    if (a.n_split == 1) a.lse[lse_idx] = l2 * kLn2;
+    else a.part_lse[lse_idx] = l2;
+  }
+}
+
+template <int KV>
+hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
+  const dim3 grid(a.n_split, a.q_len * a.Hq, a.batch);
+  switch (a.D) {
+    case 64: hipLaunchKernelGGL((attn_generic_kernel<KV, 64>), grid, dim3(64), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((attn_generic_kernel<KV, 128>), grid, dim3(64), 0, s, a); break;
+    case 256: hipLaunchKernelGGL((attn_generic_kernel<KV, 256>), grid, dim3(64), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_generic(const AttnArgs &a, hipStream_t s) {
+  switch (a.kv_type) {
+    case kF32: return launch_kv<kF32>(a, s);
+    case kBF16: return launch_kv<kBF16>(a, s);
+    case kFP8: return launch_kv<kFP8>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace kap

@@ -1,0 +1,367 @@
+// Selected-view decode (q_prop = 1) for bf16 / fp8 KV, head_dim 128, four
+// query heads per KV head -- the proposal step of Sec. 3.2 of the paper.
+//
+// Work decomposition: one 256-thread workgroup per (key split, KV head,
+// sequence). Its four wavefronts take the split's view pages round-robin, keep
+// their own online-softmax state, and merge through LDS at the end. With more
+// than one split the result is a partial (o, lse) that merge.hip combines.
+//
+// Per page (16 tokens x 128 dims = 4 KB of bf16 K and 4 KB of V^T):
+//  * K phase: lane (t = lane/4, c = lane%4) loads dims {32i + 8c .. +7}, i<4,
+//    of token t (four 16-byte loads; each instruction reads 64 contiguous
+//    bytes of every token row) and forms partial dot products for the four
+//    query heads with v_dot2_f32_bf16. A transposing reduction inside each
+//    lane quad leaves lane (t, c) holding the full logit of token t, head c.
+//  * softmax: page maxima per head come from row rotations plus permlane16 /
+//    permlane32 swaps; the running max, rescale factor and sum are kept per
+//    head in every lane that owns that head.
+//  * V phase: the V^T page is read as four contiguous 1 KB rows of 16-byte
+//    loads; lane owns dims {32i + lane/2} for tokens 8*(lane%2) .. +7, takes
+//    the probabilities of those tokens from LDS and accumulates o in fp32.
+// Everything is memory-bound: 4 flop per KV byte against a VALU ridge of
+// ~20 flop/byte, so no matrix cores are used here.
+#include "kap_internal.h"
+
+namespace kap {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kD = 128;
+constexpr int kWaves = 4;
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
+                                         __builtin_bit_cast(bf16x2, b), c, false);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kRowRor4 = 0x124;
+constexpr int kRowRor8 = 0x128;
+
+__device__ __forceinline__ float xor16_max(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return fmaxf(__int_as_float(r[0]), __int_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return fmaxf(__int_as_float(r[0]), __int_as_float(r[1]));
+}
+__device__ __forceinline__ float xor16_sum(float x) {
+  auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return __int_as_float(r[0]) + __int_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
+  return __int_as_float(r[0]) + __int_as_float(r[1]);
+}
+
+// pack the upper halves of two floats (exact bf16 values) into bf16x2
+__device__ __forceinline__ uint32_t pack_bf16_exact(float lo, float hi) {
+  return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+}
+
+// Raw registers of one page: K slice and V^T slice of this lane.
+template <int KV> struct PageRegs;
+template <> struct PageRegs<kBF16> { u32x4 k[4]; u32x4 v[4]; };
+template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x2 v[4]; };
+
+template <int KV>
+__device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, int page, int g,
+                                          int lane) {
+  const int t = lane >> 2, c = lane & 3;
+  if constexpr (KV == kBF16) {
+    const uint16_t *kb = static_cast<const uint16_t *>(a.k_pages) +
+                         ((size_t)page * a.Hkv + g) * (kPage * kD);
+    const uint16_t *vb = static_cast<const uint16_t *>(a.v_pages) +
+                         ((size_t)page * a.Hkv + g) * (kPage * kD);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      r.k[i] = *reinterpret_cast<const u32x4 *>(kb + t * kD + i * 32 + c * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      r.v[i] = *reinterpret_cast<const u32x4 *>(vb + i * 512 + lane * 8);
+  } else {
+    const uint8_t *kb = static_cast<const uint8_t *>(a.k_pages) +
+                        ((size_t)page * a.Hkv + g) * (kPage * kD);
+    const uint8_t *vb = static_cast<const uint8_t *>(a.v_pages) +
+                        ((size_t)page * a.Hkv + g) * (kPage * kD);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      r.k[i] = *reinterpret_cast<const u32x2 *>(kb + t * kD + i * 32 + c * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      r.v[i] = *reinterpret_cast<const u32x2 *>(vb + i * 512 + lane * 8);
+  }
+}
+
+// K slice of this lane as bf16 pairs: kk[i][w] holds dims 32i + 8c + 2w, +1.
+template <int KV>
+__device__ __forceinline__ void k_pairs(const PageRegs<KV> &r, uint32_t kk[4][4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (KV == kBF16) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) kk[i][w] = r.k[i][w];
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float2 f0 = fp8x2_to_f32<false>(r.k[i][h]);
+        const float2 f1 = fp8x2_to_f32<true>(r.k[i][h]);
+        kk[i][2 * h] = pack_bf16_exact(f0.x, f0.y);
+        kk[i][2 * h + 1] = pack_bf16_exact(f1.x, f1.y);
+      }
+    }
+  }
+}
+
+// V^T slice as floats: vv[i][j] = V[token 8*(lane%2) + j][dim 32i + lane/2].
+template <int KV>
+__device__ __forceinline__ void v_floats(const PageRegs<KV> &r, float vv[4][8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if constexpr (KV == kBF16) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        vv[i][2 * w] = bf16_lo(r.v[i][w]);
+        vv[i][2 * w + 1] = bf16_hi(r.v[i][w]);
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float2 f0 = fp8x2_to_f32<false>(r.v[i][h]);
+        const float2 f1 = fp8x2_to_f32<true>(r.v[i][h]);
+        vv[i][4 * h + 0] = f0.x;
+        vv[i][4 * h + 1] = f0.y;
+        vv[i][4 * h + 2] = f1.x;
+        vv[i][4 * h + 3] = f1.y;
+      }
+    }
+  }
+}
+
+template <int KV>
+__global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
+  __shared__ float pbuf[kWaves][64];
+  __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
+  __shared__ float wacc[kWaves][4][kD];
+
+  const int split = blockIdx.x;
+  const int g = blockIdx.y;
+  const int b = blockIdx.z;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int t = lane >> 2, c = lane & 3, hf = lane & 1;
+
+  const int L = a.seq_lens[b];
+  int nb = a.num_blocks[b];
+  nb = max(0, min(nb, a.max_blocks));
+  const int k0 = split * a.pages_per_split;
+  const int k1 = min(nb, k0 + a.pages_per_split);
+  const int32_t *vbt = a.block_table + (size_t)b * a.bt_stride;
+  const int32_t *vlb = a.logical_block + (size_t)b * a.bt_stride;
+
+  // query slices of the four heads, as bf16 pairs matching the K slice
+  uint32_t qr[4][4][4];
+  {
+    const uint16_t *qb = static_cast<const uint16_t *>(a.q) + ((size_t)b * a.Hq + g * 4) * kD;
+#pragma unroll
+    for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(qb + hh * kD + i * 32 + c * 8);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) qr[hh][i][w] = v[w];
+      }
+  }
+
+  float m_c = -INFINITY;     // running max (log2 units) of head c
+  float l_c = 0.f;           // partial sum of p over this lane's tokens, head c
+  float acc[4][4];           // [head][dim i] over this lane's token half
+#pragma unroll
+  for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[hh][i] = 0.f;
+
+  auto page_info = [&](int k, int &page, int &nvalid) {
+    page = vbt[k];
+    const long long rem = (long long)L - (long long)vlb[k] * kPage;
+    nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
+    if (page < 0 || (int64_t)page >= a.num_pages) nvalid = 0;
+  };
+
+  int k = k0 + wave;
+  int page = 0, nvalid = 0;
+  PageRegs<KV> cur;
+  if (k < k1) {
+    page_info(k, page, nvalid);
+    if (nvalid > 0) load_page<KV>(cur, a, page, g, lane);
+  }
+  while (k < k1) {
+    const int kn = k + kWaves;
+    int npage = 0, nnvalid = 0;
+    PageRegs<KV> nxt;
+    if (kn < k1) {
+      page_info(kn, npage, nnvalid);
+      if (nnvalid > 0) load_page<KV>(nxt, a, npage, g, lane);
+    }
+    if (nvalid > 0) {
+      float ksc = a.scale_log2, vsc = 1.f;
+      if constexpr (KV == kFP8) {
+        ksc *= a.kv_scales[2 * (size_t)page];
+        vsc = a.kv_scales[2 * (size_t)page + 1];
+      }
+      // ---- logits ------------------------------------------------------------
+      uint32_t kk[4][4];
+      k_pairs<KV>(cur, kk);
+      float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          d0 = dot2(kk[i][w], qr[0][i][w], d0);
+          d1 = dot2(kk[i][w], qr[1][i][w], d1);
+          d2 = dot2(kk[i][w], qr[2][i][w], d2);
+          d3 = dot2(kk[i][w], qr[3][i][w], d3);
+        }
+      // transposing reduction inside the quad: lane c ends with head c
+      const bool o1 = c & 1, o2 = c & 2;
+      float keep0 = o1 ? d1 : d0, send0 = o1 ? d0 : d1;
+      float keep1 = o1 ? d3 : d2, send1 = o1 ? d2 : d3;
+      keep0 += dpp<kQuadXor1>(send0);
+      keep1 += dpp<kQuadXor1>(send1);
+      float s = o2 ? keep1 : keep0;
+      s += dpp<kQuadXor2>(o2 ? keep0 : keep1);
+      s = (t < nvalid) ? s * ksc : -INFINITY;
+
+      // ---- online softmax --------------------------------------------------
+      float pm = fmaxf(s, dpp<kRowRor4>(s));
+      pm = fmaxf(pm, dpp<kRowRor8>(pm));
+      pm = xor16_max(pm);
+      pm = xor32_max(pm);
+      const float m_new = fmaxf(m_c, pm);
+      if (__any(m_new > m_c)) {
+        const float alpha = exp2f(m_c - (m_new == -INFINITY ? 0.f : m_new));
+        l_c *= alpha;
+        float al[4];
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh)
+          al[hh] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), hh));
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc[hh][i] *= al[hh];
+        m_c = m_new;
+      }
+      const float p = exp2f(s - (m_c == -INFINITY ? 0.f : m_c));
+      l_c += p;
+      pbuf[wave][lane] = p * vsc;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+      // ---- o += p V ----------------------------------------------------------
+      float vv[4][8];
+      v_floats<KV>(cur, vv);
+      if (nvalid < kPage) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const bool ok = hf * 8 + j < nvalid;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) vv[i][j] = ok ? vv[i][j] : 0.f;
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float4 pj = *reinterpret_cast<const float4 *>(&pbuf[wave][(hf * 8 + j) * 4]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          acc[0][i] = fmaf(pj.x, vv[i][j], acc[0][i]);
+          acc[1][i] = fmaf(pj.y, vv[i][j], acc[1][i]);
+          acc[2][i] = fmaf(pj.z, vv[i][j], acc[2][i]);
+          acc[3][i] = fmaf(pj.w, vv[i][j], acc[3][i]);
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    k = kn;
+    page = npage;
+    nvalid = nnvalid;
+    cur = nxt;
+  }
+
+  // ---- per-wave totals -------------------------------------------------------
+  float lt = l_c + dpp<kRowRor4>(l_c);
+  lt += dpp<kRowRor8>(lt);
+  lt = xor16_sum(lt);
+  lt = xor32_sum(lt);
+#pragma unroll
+  for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[hh][i] += dpp<kQuadXor1>(acc[hh][i]);
+  if (lane < 4) {
+    wstat[0][wave][lane] = m_c;
+    wstat[1][wave][lane] = lt;
+  }
+  if (hf == 0) {
+#pragma unroll
+    for (int hh = 0; hh < 4; ++hh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wacc[wave][hh][i * 32 + (lane >> 1)] = acc[hh][i];
+  }
+  __syncthreads();
+
+  // ---- merge the four wavefronts ------------------------------------------------
+  const int hh = threadIdx.x >> 6;
+  const int d0 = (threadIdx.x & 63) * 2;
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wstat[0][w][hh]);
+  const size_t row = (size_t)b * a.Hq + g * 4 + hh;
+  float o0 = 0.f, o1v = 0.f, lse2 = -INFINITY;
+  if (M != -INFINITY) {
+    float den = 0.f, n0 = 0.f, n1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float e = exp2f(wstat[0][w][hh] - M);
+      den = fmaf(e, wstat[1][w][hh], den);
+      n0 = fmaf(e, wacc[w][hh][d0], n0);
+      n1 = fmaf(e, wacc[w][hh][d0 + 1], n1);
+    }
+    o0 = n0 / den;
+    o1v = n1 / den;
+    lse2 = M + log2f(den);
+  }
+  if (a.n_split == 1) {
+    *reinterpret_cast<float2 *>(a.out + row * kD + d0) = make_float2(o0, o1v);
+    if ((threadIdx.x & 63) == 0) a.lse[row] = lse2 * kLn2;
+  } else {
+    const size_t pr = row * a.n_split + split;
+    *reinterpret_cast<float2 *>(a.part_o + pr * kD + d0) = make_float2(o0, o1v);
+    if ((threadIdx.x & 63) == 0) a.part_lse[pr] = lse2;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s) {
+  const dim3 grid(a.n_split, a.Hkv, a.batch);
+  if (a.kv_type == kBF16)
+    hipLaunchKernelGGL(decode_fast_kernel<kBF16>, grid, dim3(256), 0, s, a);
+  else if (a.kv_type == kFP8)
+    hipLaunchKernelGGL(decode_fast_kernel<kFP8>, grid, dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace kap

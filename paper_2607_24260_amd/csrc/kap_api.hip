@@ -1,0 +1,403 @@
+// Host side of the kap.h C ABI: argument validation, split planning,
+// workspace sizing and kernel dispatch. Nothing here allocates, frees or
+// synchronises; every launch goes to the caller's stream.
+#include "kap.h"
+
+#include <cstdarg>
+#include <cstdio>
+#include <mutex>
+#include <string>
+
+#include "kap_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+kap_status fail(kap_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+kap_status ok() {
+  g_last_error.clear();
+  return KAP_OK;
+}
+
+bool aligned(const void *p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+size_t round_up(size_t x, size_t m) { return (x + m - 1) / m * m; }
+
+// Compute units of the current device (cached per device).
+int device_cus() {
+  static std::mutex mu;
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cache[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+      v = 256;
+    cache[dev] = v;
+  }
+  return cache[dev];
+}
+
+// ---------------------------------------------------------------------------
+// KV cache / geometry checks
+// ---------------------------------------------------------------------------
+
+kap_status check_kv(const kap_kv_cache *kv) {
+  if (!kv) return fail(KAP_ERR_INVALID_ARGUMENT, "kv is NULL");
+  if (kv->num_q_heads <= 0 || kv->num_kv_heads <= 0 || kv->num_q_heads % kv->num_kv_heads)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)",
+                kv->num_q_heads, kv->num_kv_heads);
+  if (kv->page_size != 16) return fail(KAP_ERR_UNSUPPORTED, "page_size %d unsupported (16 only)", kv->page_size);
+  if (kv->head_dim != 64 && kv->head_dim != 128 && kv->head_dim != 256)
+    return fail(KAP_ERR_UNSUPPORTED, "head_dim %d unsupported (64, 128, 256)", kv->head_dim);
+  const bool f32 = kv->kv_dtype == KAP_DT_F32 && kv->q_dtype == KAP_DT_F32;
+  const bool b16 = (kv->kv_dtype == KAP_DT_BF16 || kv->kv_dtype == KAP_DT_FP8_E4M3FN) &&
+                   kv->q_dtype == KAP_DT_BF16;
+  if (!f32 && !b16)
+    return fail(KAP_ERR_UNSUPPORTED, "dtype pair kv=%d q=%d unsupported", kv->kv_dtype, kv->q_dtype);
+  if (kv->num_pages < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_pages < 0");
+  if (kv->num_pages > 0 && (!kv->k_pages || !kv->v_pages))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "k_pages / v_pages is NULL");
+  if (!aligned(kv->k_pages, 16) || !aligned(kv->v_pages, 16))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "k_pages / v_pages must be 16-byte aligned");
+  if (kv->kv_dtype == KAP_DT_FP8_E4M3FN && kv->num_pages > 0 && !kv->kv_scales)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "FP8 KV needs kv_scales");
+  return KAP_OK;
+}
+
+bool fast_geometry(const kap_kv_cache *kv) {
+  return kv->q_dtype == KAP_DT_BF16 &&
+         (kv->kv_dtype == KAP_DT_BF16 || kv->kv_dtype == KAP_DT_FP8_E4M3FN) &&
+         kv->head_dim == 128 && kv->num_q_heads == 4 * kv->num_kv_heads;
+}
+
+struct SplitPlan {
+  bool fast;
+  int n_split;
+  int pps;  // pages per split
+};
+
+int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+// Decode: fast path uses 4-wavefront workgroups, ~2 per CU; generic path caps
+// each split at kGenericPagesPerSplit pages.
+SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num_splits) {
+  SplitPlan p{fast_geometry(kv), 1, 1};
+  const int mb = max_blocks > 0 ? max_blocks : 1;
+  if (p.fast) {
+    int n;
+    if (num_splits > 0) {
+      n = num_splits;
+    } else {
+      const long long work = (long long)batch * kv->num_kv_heads;
+      n = cdiv(2LL * device_cus(), work > 0 ? work : 1);
+      n = n < cdiv(mb, 4) ? n : cdiv(mb, 4);
+    }
+    n = n < 1 ? 1 : (n > mb ? mb : n);
+    p.pps = cdiv(mb, n);
+    p.n_split = cdiv(mb, p.pps);
+  } else {
+    int n = cdiv(mb, kap::kGenericPagesPerSplit);
+    if (num_splits > n) n = num_splits > mb ? mb : num_splits;
+    p.pps = cdiv(mb, n);
+    p.n_split = cdiv(mb, p.pps);
+  }
+  return p;
+}
+
+// Verify: fast path uses one wavefront per split, ~8 per CU; pages per split
+// are even (the kernel walks page pairs).
+SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_pages, int num_splits) {
+  SplitPlan p{fast_geometry(kv) && q_len * 4 <= 64, 1, 1};
+  const int mp = max_pages > 0 ? max_pages : 1;
+  if (p.fast) {
+    const int pairs = cdiv(mp, 2);
+    int n;
+    if (num_splits > 0) {
+      n = num_splits;
+    } else {
+      const long long work = (long long)batch * kv->num_kv_heads;
+      n = cdiv(8LL * device_cus(), work > 0 ? work : 1);
+    }
+    n = n < 1 ? 1 : (n > pairs ? pairs : n);
+    p.pps = 2 * cdiv(pairs, n);
+    p.n_split = cdiv(mp, p.pps);
+  } else {
+    int n = cdiv(mp, kap::kGenericPagesPerSplit);
+    if (num_splits > n) n = num_splits > mp ? mp : num_splits;
+    p.pps = cdiv(mp, n);
+    p.n_split = cdiv(mp, p.pps);
+  }
+  return p;
+}
+
+size_t partial_bytes(const kap_kv_cache *kv, int batch, int q_len, const SplitPlan &p) {
+  if (p.n_split <= 1 || batch <= 0) return 0;
+  const size_t rows = (size_t)batch * q_len * kv->num_q_heads;
+  const size_t o = round_up(rows * p.n_split * kv->head_dim * sizeof(float), 256);
+  const size_t l = round_up(rows * p.n_split * sizeof(float), 256);
+  return o + l;
+}
+
+kap_status launch_attention(kap::AttnArgs &a, const SplitPlan &p, bool decode, void *ws,
+                            hipStream_t s) {
+  a.n_split = p.n_split;
+  a.pages_per_split = p.pps;
+  const size_t rows = (size_t)a.batch * a.q_len * a.Hq;
+  a.part_o = static_cast<float *>(ws);
+  a.part_lse = p.n_split > 1
+                   ? reinterpret_cast<float *>(static_cast<char *>(ws) +
+                                               round_up(rows * p.n_split * a.D * sizeof(float), 256))
+                   : nullptr;
+  (void)hipGetLastError();  // clear a stale error so a launch failure is ours
+  hipError_t e;
+  if (p.fast)
+    e = decode ? kap::launch_decode_fast(a, s) : kap::launch_verify_mfma(a, s);
+  else
+    e = kap::launch_attn_generic(a, s);
+  if (e == hipSuccess && p.n_split > 1) e = kap::launch_merge(a, s);
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *kap_status_string(kap_status s) {
+  switch (s) {
+    case KAP_OK: return "KAP_OK";
+    case KAP_ERR_INVALID_ARGUMENT: return "KAP_ERR_INVALID_ARGUMENT";
+    case KAP_ERR_UNSUPPORTED: return "KAP_ERR_UNSUPPORTED";
+    case KAP_ERR_WORKSPACE_TOO_SMALL: return "KAP_ERR_WORKSPACE_TOO_SMALL";
+    case KAP_ERR_HIP: return "KAP_ERR_HIP";
+    default: return "KAP_UNKNOWN_STATUS";
+  }
+}
+
+const char *kap_last_error(void) { return g_last_error.c_str(); }
+
+int32_t kap_abi_version(void) { return KAP_ABI_VERSION; }
+
+// ---------------------------------------------------------------------------
+// kap_compile_plan
+// ---------------------------------------------------------------------------
+
+size_t kap_compile_plan_workspace_bytes(int32_t batch, int32_t num_spans, int32_t fbt_stride) {
+  (void)batch;
+  (void)fbt_stride;
+  return num_spans > 0 ? round_up((size_t)num_spans * sizeof(int32_t), 256) : 0;
+}
+
+kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens, const int32_t *full_block_table,
+                            int32_t fbt_stride, const int32_t *span_offsets, int32_t num_spans,
+                            const int32_t *span_start, const int32_t *span_len,
+                            const float *span_prior, const int32_t *prefix_tokens,
+                            const int32_t *suffix_tokens, const int32_t *budget_tokens,
+                            kap_select_policy policy, int64_t num_pages, int32_t view_capacity,
+                            int32_t *view_block_table, int32_t *view_logical_block,
+                            int32_t *view_num_blocks, int32_t *view_tokens, int32_t *spans_taken,
+                            int32_t *plan_status, int32_t *span_selected, void *workspace,
+                            size_t workspace_bytes, void *stream) {
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (num_spans < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_spans < 0");
+  if (view_capacity < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "view_capacity < 0");
+  if (num_pages < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_pages < 0");
+  if (policy != KAP_SELECT_SKIP && policy != KAP_SELECT_STOP)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "unknown selection policy %d", policy);
+  if (fbt_stride < 1) return fail(KAP_ERR_INVALID_ARGUMENT, "fbt_stride < 1");
+  if (fbt_stride > kap::kMaxPlanPages)
+    return fail(KAP_ERR_UNSUPPORTED, "fbt_stride %d exceeds %d pages", fbt_stride, kap::kMaxPlanPages);
+  if (batch == 0) return ok();
+  if (!seq_lens || !full_block_table || !span_offsets || !prefix_tokens || !suffix_tokens ||
+      !budget_tokens || !view_num_blocks || !view_tokens || !spans_taken || !plan_status)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (num_spans > 0 && (!span_start || !span_len || !span_prior))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "span arrays are NULL");
+  if (view_capacity > 0 && (!view_block_table || !view_logical_block))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "view tables are NULL");
+  const size_t need = kap_compile_plan_workspace_bytes(batch, num_spans, fbt_stride);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+
+  kap::PlanArgs a;
+  a.batch = batch;
+  a.seq_lens = seq_lens;
+  a.fbt = full_block_table;
+  a.fbt_stride = fbt_stride;
+  a.span_offsets = span_offsets;
+  a.num_spans = num_spans;
+  a.span_start = span_start;
+  a.span_len = span_len;
+  a.span_prior = span_prior;
+  a.prefix = prefix_tokens;
+  a.suffix = suffix_tokens;
+  a.budget = budget_tokens;
+  a.policy = policy;
+  a.num_pages = num_pages;
+  a.capacity = view_capacity;
+  a.view_bt = view_block_table;
+  a.view_lblk = view_logical_block;
+  a.view_nblk = view_num_blocks;
+  a.view_tokens = view_tokens;
+  a.spans_taken = spans_taken;
+  a.status = plan_status;
+  a.span_selected = span_selected;
+  a.perm = static_cast<int32_t *>(workspace);
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_compile_plan(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "compile_plan launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+// ---------------------------------------------------------------------------
+// kap_selected_decode
+// ---------------------------------------------------------------------------
+
+size_t kap_selected_decode_workspace_bytes(const kap_kv_cache *kv, int32_t batch,
+                                           int32_t max_view_blocks, int32_t num_splits) {
+  if (check_kv(kv) != KAP_OK || batch <= 0 || max_view_blocks < 0) return 0;
+  const SplitPlan p = plan_decode(kv, batch, max_view_blocks, num_splits);
+  return partial_bytes(kv, batch, 1, p);
+}
+
+kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void *q,
+                               const int32_t *seq_lens, const int32_t *view_block_table,
+                               const int32_t *view_logical_block, int32_t view_stride,
+                               const int32_t *view_num_blocks, int32_t max_view_blocks,
+                               float sm_scale, int32_t num_splits, float *out, float *lse,
+                               void *workspace, size_t workspace_bytes, void *stream) {
+  kap_status st = check_kv(kv);
+  if (st != KAP_OK) return st;
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (batch > 65535) return fail(KAP_ERR_UNSUPPORTED, "batch %d > 65535", batch);
+  if (max_view_blocks < 0 || view_stride < max_view_blocks)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "need 0 <= max_view_blocks (%d) <= view_stride (%d)",
+                max_view_blocks, view_stride);
+  if (num_splits < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_splits < 0");
+  if (!(sm_scale == sm_scale) || sm_scale > 3.0e38f || sm_scale < -3.0e38f)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "sm_scale must be finite");
+  if (kv->num_q_heads > 65535) return fail(KAP_ERR_UNSUPPORTED, "too many query heads");
+  if (batch == 0) return ok();
+  if (!q || !seq_lens || !view_num_blocks || !out || !lse)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (max_view_blocks > 0 && (!view_block_table || !view_logical_block))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "view tables are NULL");
+  if (!aligned(q, 16) || !aligned(out, 16))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "q and out must be 16-byte aligned");
+  const SplitPlan p = plan_decode(kv, batch, max_view_blocks, num_splits);
+  const size_t need = partial_bytes(kv, batch, 1, p);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (need > 0 && !aligned(workspace, 256))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+
+  kap::AttnArgs a;
+  a.batch = batch;
+  a.Hq = kv->num_q_heads;
+  a.Hkv = kv->num_kv_heads;
+  a.G = kv->num_q_heads / kv->num_kv_heads;
+  a.D = kv->head_dim;
+  a.kv_type = kv->kv_dtype;
+  a.k_pages = kv->k_pages;
+  a.v_pages = kv->v_pages;
+  a.kv_scales = kv->kv_scales;
+  a.num_pages = kv->num_pages;
+  a.q = q;
+  a.q_f32 = kv->q_dtype == KAP_DT_F32;
+  a.q_len = 1;
+  a.seq_lens = seq_lens;
+  a.block_table = view_block_table;
+  a.bt_stride = view_stride;
+  a.logical_block = view_logical_block;
+  a.num_blocks = view_num_blocks;
+  a.max_blocks = max_view_blocks;
+  a.causal = 0;
+  a.scale_log2 = sm_scale * kap::kLog2e;
+  a.out = out;
+  a.lse = lse;
+  return launch_attention(a, p, true, workspace, static_cast<hipStream_t>(stream));
+}
+
+// ---------------------------------------------------------------------------
+// kap_verify
+// ---------------------------------------------------------------------------
+
+size_t kap_verify_workspace_bytes(const kap_kv_cache *kv, int32_t batch, int32_t q_len,
+                                  int32_t max_seq_len, int32_t num_splits) {
+  if (check_kv(kv) != KAP_OK || batch <= 0 || q_len < 1 || q_len > 16 || max_seq_len < 0) return 0;
+  const int max_pages = cdiv(max_seq_len, 16);
+  const SplitPlan p = plan_verify(kv, batch, q_len, max_pages, num_splits);
+  return partial_bytes(kv, batch, q_len, p);
+}
+
+kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, const void *q,
+                      const int32_t *seq_lens, const int32_t *full_block_table,
+                      int32_t fbt_stride, int32_t max_seq_len, float sm_scale,
+                      int32_t num_splits, float *out, float *lse, void *workspace,
+                      size_t workspace_bytes, void *stream) {
+  kap_status st = check_kv(kv);
+  if (st != KAP_OK) return st;
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (batch > 65535) return fail(KAP_ERR_UNSUPPORTED, "batch %d > 65535", batch);
+  if (q_len < 1 || q_len > 16) return fail(KAP_ERR_INVALID_ARGUMENT, "q_len %d outside [1, 16]", q_len);
+  if (max_seq_len < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "max_seq_len < 0");
+  const int max_pages = cdiv(max_seq_len, 16);
+  if (fbt_stride < max_pages)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "fbt_stride %d < ceil(max_seq_len/16) = %d", fbt_stride, max_pages);
+  if (num_splits < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_splits < 0");
+  if (!(sm_scale == sm_scale) || sm_scale > 3.0e38f || sm_scale < -3.0e38f)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "sm_scale must be finite");
+  if ((long long)q_len * kv->num_q_heads > 65535) return fail(KAP_ERR_UNSUPPORTED, "too many rows");
+  if (batch == 0) return ok();
+  if (!q || !seq_lens || !out || !lse) return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (max_pages > 0 && !full_block_table)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "full_block_table is NULL");
+  if (!aligned(q, 16) || !aligned(out, 16))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "q and out must be 16-byte aligned");
+  const SplitPlan p = plan_verify(kv, batch, q_len, max_pages, num_splits);
+  const size_t need = partial_bytes(kv, batch, q_len, p);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (need > 0 && !aligned(workspace, 256))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+
+  kap::AttnArgs a;
+  a.batch = batch;
+  a.Hq = kv->num_q_heads;
+  a.Hkv = kv->num_kv_heads;
+  a.G = kv->num_q_heads / kv->num_kv_heads;
+  a.D = kv->head_dim;
+  a.kv_type = kv->kv_dtype;
+  a.k_pages = kv->k_pages;
+  a.v_pages = kv->v_pages;
+  a.kv_scales = kv->kv_scales;
+  a.num_pages = kv->num_pages;
+  a.q = q;
+  a.q_f32 = kv->q_dtype == KAP_DT_F32;
+  a.q_len = q_len;
+  a.seq_lens = seq_lens;
+  a.block_table = full_block_table;
+  a.bt_stride = fbt_stride;
+  a.logical_block = nullptr;
+  a.num_blocks = nullptr;
+  a.max_blocks = max_pages;
+  a.causal = 1;
+  a.scale_log2 = sm_scale * kap::kLog2e;
+  a.out = out;
+  a.lse = lse;
+  return launch_attention(a, p, false, workspace, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,223 @@
+// kap_compile_plan on the GPU: Alg. 1 of the paper, SelectEvidenceUnderBudget
+// through BuildBlockTable, one workgroup per sequence.
+//
+// Per sequence the workgroup
+//   1. checks the CSR bounds, the length and the scores (status codes),
+//   2. marks the mandatory prefix / suffix pages in an LDS page bitmap,
+//   3. ranks the spans by (prior desc, start asc, index asc) -- every thread
+//      counts, for its spans, how many spans precede them, and writes the
+//      inverse permutation to the workspace,
+//   4. walks the spans in rank order with one wavefront: the 64 lanes test the
+//      span's pages against the bitmap, a wavefront sum gives the cost in
+//      visible tokens, and the span is taken when it fits the budget,
+//   5. compacts the bitmap into the ascending logical-page list and maps it
+//      through the full block table.
+// Selection uses integer arithmetic only (float priors are only compared), so
+// the plan is bit-for-bit deterministic.
+#include "kap_internal.h"
+
+namespace kap {
+namespace {
+
+__device__ __forceinline__ bool ranks_before(float pj, int sj, int j, float pi, int si, int i) {
+  if (pj > pi) return true;
+  if (pj < pi) return false;           // equal values (including -0 == +0) fall through
+  if (sj != si) return sj < si;
+  return j < i;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) {
+  extern __shared__ uint32_t bitmap[];
+  __shared__ int s_flag;
+  __shared__ int s_count[kPlanThreads];
+  __shared__ long long s_used;
+  __shared__ int s_taken;
+
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+
+  const int lo = a.span_offsets[b];
+  const int hi = a.span_offsets[b + 1];
+
+  auto write_fail = [&](int status, bool zero_flags) {
+    if (zero_flags && a.span_selected) {
+      for (int i = lo + tid; i < hi; i += kPlanThreads) a.span_selected[i] = 0;
+    }
+    if (tid == 0) {
+      a.view_nblk[b] = 0;
+      a.view_tokens[b] = 0;
+      a.spans_taken[b] = 0;
+      a.status[b] = status;
+    }
+  };
+
+  if (lo < 0 || hi < lo || hi > a.num_spans) {
+    write_fail(5 /*KAP_PLAN_BAD_SPANS*/, false);
+    return;
+  }
+  const int L = a.seq_lens[b];
+  const int NP = (L >= 1) ? (int)(((long long)L + kPage - 1) / kPage) : 0;
+  if (L < 1 || NP > a.fbt_stride) {
+    write_fail(4 /*KAP_PLAN_BAD_LENGTH*/, true);
+    return;
+  }
+
+  // -- scores ---------------------------------------------------------------
+  if (tid == 0) s_flag = 0;
+  __syncthreads();
+  for (int i = lo + tid; i < hi; i += kPlanThreads)
+    if (__builtin_isnan(a.span_prior[i])) s_flag = 1;
+  __syncthreads();
+  if (s_flag) {
+    write_fail(2 /*KAP_PLAN_BAD_SCORE*/, true);
+    return;
+  }
+
+  // -- mandatory pages --------------------------------------------------------
+  const int W = (NP + 31) / 32;
+  for (int w = tid; w < W; w += kPlanThreads) bitmap[w] = 0u;
+  __syncthreads();
+  const int pre = min(max(a.prefix[b], 0), L);
+  const int suf_start = max(0, L - max(a.suffix[b], 1));
+  const int pre_pages = (pre + kPage - 1) / kPage;     // pages [0, pre_pages)
+  const int suf_page0 = suf_start / kPage;             // pages [suf_page0, NP)
+  for (int p = tid; p < pre_pages; p += kPlanThreads) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+  for (int p = suf_page0 + tid; p < NP; p += kPlanThreads)
+    atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+
+  // -- rank the spans ---------------------------------------------------------
+  const int n = hi - lo;
+  for (int i = tid; i < n; i += kPlanThreads) {
+    const float pi = a.span_prior[lo + i];
+    const int si = a.span_start[lo + i];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+      rank += ranks_before(a.span_prior[lo + j], a.span_start[lo + j], j, pi, si, i) ? 1 : 0;
+    }
+    a.perm[lo + rank] = i;
+    if (a.span_selected) a.span_selected[lo + i] = 0;
+  }
+  __syncthreads();
+
+  // -- visible tokens of the mandatory pages ---------------------------------
+  const int last_valid = L - kPage * (NP - 1);          // 1..16
+  {
+    int c = 0;
+    for (int w = tid; w < W; w += kPlanThreads) c += __popc(bitmap[w]);
+    s_count[tid] = c;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int c = 0;
+    for (int t = 0; t < kPlanThreads; ++t) c += s_count[t];
+    // the last page is always selected (suffix >= 1 token)
+    s_used = (long long)kPage * c - (kPage - last_valid);
+    s_taken = 0;
+  }
+  __syncthreads();
+
+  // -- greedy selection in rank order (one wavefront) -------------------------
+  if (tid < 64) {
+    long long used = s_used;
+    int taken = 0;
+    const long long T = a.budget[b];
+    for (int r = 0; r < n; ++r) {
+      const int i = lo + a.perm[lo + r];
+      const long long st = a.span_start[i];
+      const long long x = st > 0 ? st : 0;
+      long long e = st + (long long)a.span_len[i];
+      if (e > L) e = L;
+      if (e <= x) continue;                               // empty after clipping
+      const int p0 = (int)(x / kPage);
+      const int p1 = (int)((e + kPage - 1) / kPage);
+      int cost = 0;
+      for (int p = p0 + lane; p < p1; p += 64) {
+        const bool sel = (bitmap[p >> 5] >> (p & 31)) & 1u;
+        if (!sel) cost += (p == NP - 1) ? last_valid : kPage;
+      }
+      cost = wave_sum_i(cost);
+      if (used + cost <= T) {
+        for (int p = p0 + lane; p < p1; p += 64) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+        used += cost;
+        ++taken;
+        if (lane == 0 && a.span_selected) a.span_selected[i] = 1;
+      } else if (a.policy == 1 /*KAP_SELECT_STOP*/) {
+        break;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    }
+    if (lane == 0) {
+      s_used = used;
+      s_taken = taken;
+    }
+  }
+  __syncthreads();
+
+  // -- compaction: ascending logical pages -> block table ---------------------
+  const int chunk = (W + kPlanThreads - 1) / kPlanThreads;
+  const int w0 = min(W, tid * chunk);
+  const int w1 = min(W, w0 + chunk);
+  int mine = 0;
+  for (int w = w0; w < w1; ++w) mine += __popc(bitmap[w]);
+  s_count[tid] = mine;
+  if (tid == 0) s_flag = 0;
+  __syncthreads();
+  if (tid == 0) {                                         // exclusive scan (256 entries)
+    int run = 0;
+    for (int t = 0; t < kPlanThreads; ++t) {
+      const int c = s_count[t];
+      s_count[t] = run;
+      run += c;
+    }
+    s_flag = 0;
+    bitmap[W] = (uint32_t)run;                            // spare word: total count
+  }
+  __syncthreads();
+  const int nblk = (int)bitmap[W];
+  if (nblk > a.capacity) {
+    write_fail(1 /*KAP_PLAN_OVER_CAPACITY*/, true);
+    return;
+  }
+  int out = s_count[tid];
+  const int32_t *fbt_row = a.fbt + (size_t)b * a.fbt_stride;
+  int32_t *vbt = a.view_bt + (size_t)b * a.capacity;
+  int32_t *vlb = a.view_lblk + (size_t)b * a.capacity;
+  bool bad = false;
+  for (int w = w0; w < w1; ++w) {
+    uint32_t bits = bitmap[w];
+    while (bits) {
+      const int bit = __ffs(bits) - 1;
+      bits &= bits - 1u;
+      const int p = w * 32 + bit;
+      const int page = fbt_row[p];
+      bad |= (page < 0) || ((int64_t)page >= a.num_pages);
+      vlb[out] = p;
+      vbt[out] = page;
+      ++out;
+    }
+  }
+  if (bad) s_flag = 1;
+  __syncthreads();
+  if (s_flag) {
+    write_fail(3 /*KAP_PLAN_BAD_PAGE*/, true);
+    return;
+  }
+  if (tid == 0) {
+    a.view_nblk[b] = nblk;
+    a.view_tokens[b] = (int)s_used;
+    a.spans_taken[b] = s_taken;
+    a.status[b] = 0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_compile_plan(const PlanArgs &a, hipStream_t s) {
+  const size_t words = (size_t)(a.fbt_stride + 31) / 32 + 1;   // + spare count word
+  hipLaunchKernelGGL(compile_plan_kernel, dim3(a.batch), dim3(kPlanThreads),
+                     words * sizeof(uint32_t), s, a);
+  return hipGetLastError();
+}
+
+}  // namespace kap

@@ -1,0 +1,359 @@
+"""Python binding of the kap.h C ABI (argument marshalling only).
+
+Every function here checks tensor placement, dtype and shape, allocates
+outputs / workspace with torch when the caller does not pass them, and calls
+the matching ``kap_*`` entry point of ``libkap.so`` on torch's current HIP
+stream. All computation happens in the library's HIP kernels; there is no CPU
+path. A missing library or a CPU tensor raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkap.so")
+
+KAP_OK = 0
+KAP_ERR_INVALID_ARGUMENT = 1
+KAP_ERR_UNSUPPORTED = 2
+KAP_ERR_WORKSPACE_TOO_SMALL = 3
+KAP_ERR_HIP = 4
+
+KAP_DT_F32 = 0
+KAP_DT_BF16 = 1
+KAP_DT_FP8_E4M3FN = 2
+
+KAP_SELECT_SKIP = 0
+KAP_SELECT_STOP = 1
+
+KAP_PLAN_OK = 0
+KAP_PLAN_OVER_CAPACITY = 1
+KAP_PLAN_BAD_SCORE = 2
+KAP_PLAN_BAD_PAGE = 3
+KAP_PLAN_BAD_LENGTH = 4
+KAP_PLAN_BAD_SPANS = 5
+
+PAGE = 16
+
+EXPORTS = (
+    "kap_compile_plan", "kap_compile_plan_workspace_bytes",
+    "kap_selected_decode", "kap_selected_decode_workspace_bytes",
+    "kap_verify", "kap_verify_workspace_bytes",
+    "kap_status_string", "kap_last_error", "kap_abi_version",
+)
+
+
+class KapError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(message)
+        self.status = status
+
+
+class KVCacheStruct(ctypes.Structure):
+    _fields_ = [
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("kv_dtype", ctypes.c_int32),
+        ("q_dtype", ctypes.c_int32),
+        ("k_pages", ctypes.c_void_p),
+        ("v_pages", ctypes.c_void_p),
+        ("kv_scales", ctypes.c_void_p),
+        ("num_pages", ctypes.c_int64),
+    ]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+_F = ctypes.c_float
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libkap.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"libkap.so not found at {path}; build it with "
+                          f"`python -m paper_2607_24260_amd.build`")
+    lib = ctypes.CDLL(path)
+    lib.kap_compile_plan.restype = _I32
+    lib.kap_compile_plan.argtypes = [
+        _I32, _P, _P, _I32, _P, _I32, _P, _P, _P, _P, _P, _P, _I32, _I64, _I32,
+        _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.kap_compile_plan_workspace_bytes.restype = _SZ
+    lib.kap_compile_plan_workspace_bytes.argtypes = [_I32, _I32, _I32]
+    lib.kap_selected_decode.restype = _I32
+    lib.kap_selected_decode.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _I32, _P, _I32, _F, _I32,
+        _P, _P, _P, _SZ, _P]
+    lib.kap_selected_decode_workspace_bytes.restype = _SZ
+    lib.kap_selected_decode_workspace_bytes.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _I32, _I32]
+    lib.kap_verify.restype = _I32
+    lib.kap_verify.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _I32, _P, _P, _P, _I32, _I32, _F, _I32,
+        _P, _P, _P, _SZ, _P]
+    lib.kap_verify_workspace_bytes.restype = _SZ
+    lib.kap_verify_workspace_bytes.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _I32, _I32, _I32]
+    lib.kap_status_string.restype = ctypes.c_char_p
+    lib.kap_status_string.argtypes = [_I32]
+    lib.kap_last_error.restype = ctypes.c_char_p
+    lib.kap_last_error.argtypes = []
+    lib.kap_abi_version.restype = _I32
+    lib.kap_abi_version.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != KAP_OK:
+        lib = load_library()
+        raise KapError(status, f"{lib.kap_status_string(status).decode()}: "
+                               f"{lib.kap_last_error().decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device}); libkap has no CPU path")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    return t
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
+    if nbytes == 0:
+        return workspace, 0
+    if workspace is None:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    _dev(workspace, "workspace")
+    have = workspace.numel() * workspace.element_size()
+    return workspace, have
+
+
+# --------------------------------------------------------------------------
+# KV cache descriptor
+# --------------------------------------------------------------------------
+
+_KV_DT = {torch.float32: KAP_DT_F32, torch.bfloat16: KAP_DT_BF16, torch.uint8: KAP_DT_FP8_E4M3FN,
+          torch.float8_e4m3fn: KAP_DT_FP8_E4M3FN}
+_Q_DT = {torch.float32: KAP_DT_F32, torch.bfloat16: KAP_DT_BF16}
+
+
+@dataclass
+class KVCache:
+    """Paged KV pool: k_pages [P][Hkv][16][D], v_pages [P][Hkv][D][16];
+    fp8 pools are uint8 (E4M3FN codes) with kv_scales [P][2] float32."""
+    k_pages: torch.Tensor
+    v_pages: torch.Tensor
+    num_q_heads: int
+    q_dtype: torch.dtype
+    kv_scales: Optional[torch.Tensor] = None
+
+    def __post_init__(self):
+        _dev(self.k_pages, "k_pages", ndim=4)
+        _dev(self.v_pages, "v_pages", ndim=4)
+        P, Hkv, page, D = self.k_pages.shape
+        if tuple(self.v_pages.shape) != (P, Hkv, D, page):
+            raise ValueError(f"v_pages must be [P][Hkv][D][page] = {(P, Hkv, D, page)}, "
+                             f"got {tuple(self.v_pages.shape)}")
+        if self.k_pages.dtype != self.v_pages.dtype or self.k_pages.dtype not in _KV_DT:
+            raise TypeError("k_pages / v_pages must share a float32, bfloat16 or uint8 dtype")
+        if self.q_dtype not in _Q_DT:
+            raise TypeError("q_dtype must be float32 or bfloat16")
+        if _KV_DT[self.k_pages.dtype] == KAP_DT_FP8_E4M3FN:
+            if self.kv_scales is None:
+                raise ValueError("fp8 KV needs kv_scales [P][2]")
+            _dev(self.kv_scales, "kv_scales", torch.float32)
+            if tuple(self.kv_scales.shape) != (P, 2):
+                raise ValueError("kv_scales must be [num_pages][2]")
+        self.num_kv_heads = Hkv
+        self.head_dim = D
+        self.page_size = page
+        self.num_pages = P
+        self.struct = KVCacheStruct(
+            self.num_q_heads, Hkv, D, page, _KV_DT[self.k_pages.dtype], _Q_DT[self.q_dtype],
+            self.k_pages.data_ptr(), self.v_pages.data_ptr(),
+            self.kv_scales.data_ptr() if self.kv_scales is not None else None, P)
+
+    @property
+    def device(self):
+        return self.k_pages.device
+
+
+# --------------------------------------------------------------------------
+# kap_compile_plan
+# --------------------------------------------------------------------------
+
+def compile_plan_workspace_bytes(batch: int, num_spans: int, fbt_stride: int) -> int:
+    return int(load_library().kap_compile_plan_workspace_bytes(batch, num_spans, fbt_stride))
+
+
+def compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
+                 prefix_tokens, suffix_tokens, budget_tokens, *, num_pages: int,
+                 view_capacity: int, policy: int = KAP_SELECT_SKIP, out: Optional[dict] = None,
+                 workspace: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """Runtime access plan of every sequence (Alg. 1). Returns a dict of GPU
+    tensors: view_block_table, view_logical_block [B][view_capacity],
+    view_num_blocks, view_tokens, spans_taken, plan_status [B], span_selected [S]."""
+    lib = load_library()
+    i32 = torch.int32
+    _dev(seq_lens, "seq_lens", i32, 1)
+    B = seq_lens.shape[0]
+    _dev(full_block_table, "full_block_table", i32, 2)
+    if full_block_table.shape[0] != B:
+        raise ValueError("full_block_table must have one row per sequence")
+    _dev(span_offsets, "span_offsets", i32, 1)
+    if span_offsets.shape[0] != B + 1:
+        raise ValueError("span_offsets must have batch+1 entries")
+    for name, t, dt in (("span_start", span_start, i32), ("span_len", span_len, i32),
+                        ("span_prior", span_prior, torch.float32)):
+        _dev(t, name, dt, 1)
+    S = span_start.shape[0]
+    if span_len.shape[0] != S or span_prior.shape[0] != S:
+        raise ValueError("span arrays must have equal length")
+    for name, t in (("prefix_tokens", prefix_tokens), ("suffix_tokens", suffix_tokens),
+                    ("budget_tokens", budget_tokens)):
+        _dev(t, name, i32, 1)
+        if t.shape[0] != B:
+            raise ValueError(f"{name} must have batch entries")
+    dev = seq_lens.device
+    if out is None:
+        cap = max(int(view_capacity), 0)
+        out = {
+            "view_block_table": torch.empty((B, cap), dtype=i32, device=dev),
+            "view_logical_block": torch.empty((B, cap), dtype=i32, device=dev),
+            "view_num_blocks": torch.empty(B, dtype=i32, device=dev),
+            "view_tokens": torch.empty(B, dtype=i32, device=dev),
+            "spans_taken": torch.empty(B, dtype=i32, device=dev),
+            "plan_status": torch.empty(B, dtype=i32, device=dev),
+            "span_selected": torch.empty(S, dtype=i32, device=dev),
+        }
+    for name in ("view_block_table", "view_logical_block"):
+        _dev(out[name], name, i32, 2)
+        if out[name].shape != (B, view_capacity):
+            raise ValueError(f"{name} must be [batch][view_capacity]")
+    need = compile_plan_workspace_bytes(B, S, full_block_table.shape[1])
+    workspace, have = _workspace(need, dev, workspace)
+    st = lib.kap_compile_plan(
+        B, _ptr(seq_lens), _ptr(full_block_table), full_block_table.shape[1], _ptr(span_offsets),
+        S, _ptr(span_start), _ptr(span_len), _ptr(span_prior), _ptr(prefix_tokens),
+        _ptr(suffix_tokens), _ptr(budget_tokens), int(policy), int(num_pages), int(view_capacity),
+        _ptr(out["view_block_table"]), _ptr(out["view_logical_block"]),
+        _ptr(out["view_num_blocks"]), _ptr(out["view_tokens"]), _ptr(out["spans_taken"]),
+        _ptr(out["plan_status"]), _ptr(out.get("span_selected")), _ptr(workspace), have,
+        _stream(stream))
+    _check(st)
+    return out
+
+
+# --------------------------------------------------------------------------
+# kap_selected_decode / kap_verify
+# --------------------------------------------------------------------------
+
+def selected_decode_workspace_bytes(kv: KVCache, batch: int, max_view_blocks: int,
+                                    num_splits: int = 0) -> int:
+    return int(load_library().kap_selected_decode_workspace_bytes(
+        ctypes.byref(kv.struct), batch, max_view_blocks, num_splits))
+
+
+def verify_workspace_bytes(kv: KVCache, batch: int, q_len: int, max_seq_len: int,
+                           num_splits: int = 0) -> int:
+    return int(load_library().kap_verify_workspace_bytes(
+        ctypes.byref(kv.struct), batch, q_len, max_seq_len, num_splits))
+
+
+def _outputs(shape, dev, out, lse):
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=dev)
+    if lse is None:
+        lse = torch.empty(shape[:-1], dtype=torch.float32, device=dev)
+    _dev(out, "out", torch.float32)
+    _dev(lse, "lse", torch.float32)
+    if tuple(out.shape) != tuple(shape) or tuple(lse.shape) != tuple(shape[:-1]):
+        raise ValueError(f"out must be {tuple(shape)} and lse {tuple(shape[:-1])}")
+    return out, lse
+
+
+def selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
+                    view_num_blocks, max_view_blocks: int, sm_scale: float, *,
+                    num_splits: int = 0, out=None, lse=None, workspace=None, stream=None):
+    """One proposal step over the selected-KV view. q [B][Hq][D]; returns
+    (out [B][Hq][D] float32, lse [B][Hq] float32)."""
+    lib = load_library()
+    _dev(q, "q", kv.q_dtype, 3)
+    B = q.shape[0]
+    if tuple(q.shape[1:]) != (kv.num_q_heads, kv.head_dim):
+        raise ValueError("q must be [batch][num_q_heads][head_dim]")
+    _dev(seq_lens, "seq_lens", torch.int32, 1)
+    _dev(view_num_blocks, "view_num_blocks", torch.int32, 1)
+    _dev(view_block_table, "view_block_table", torch.int32, 2)
+    _dev(view_logical_block, "view_logical_block", torch.int32, 2)
+    if view_block_table.shape != view_logical_block.shape or view_block_table.shape[0] != B:
+        raise ValueError("view tables must both be [batch][view_stride]")
+    if seq_lens.shape[0] != B or view_num_blocks.shape[0] != B:
+        raise ValueError("seq_lens / view_num_blocks must have batch entries")
+    out, lse = _outputs((B, kv.num_q_heads, kv.head_dim), q.device, out, lse)
+    need = selected_decode_workspace_bytes(kv, B, max_view_blocks, num_splits)
+    workspace, have = _workspace(need, q.device, workspace)
+    st = lib.kap_selected_decode(
+        ctypes.byref(kv.struct), B, _ptr(q), _ptr(seq_lens), _ptr(view_block_table),
+        _ptr(view_logical_block), view_block_table.shape[1], _ptr(view_num_blocks),
+        int(max_view_blocks), float(sm_scale), int(num_splits), _ptr(out), _ptr(lse),
+        _ptr(workspace), have, _stream(stream))
+    _check(st)
+    return out, lse
+
+
+def verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scale: float, *,
+           num_splits: int = 0, out=None, lse=None, workspace=None, stream=None):
+    """Causal attention of the verify window over the full KV. q [B][q_len][Hq][D];
+    returns (out [B][q_len][Hq][D] float32, lse [B][q_len][Hq] float32)."""
+    lib = load_library()
+    _dev(q, "q", kv.q_dtype, 4)
+    B, q_len = q.shape[0], q.shape[1]
+    if tuple(q.shape[2:]) != (kv.num_q_heads, kv.head_dim):
+        raise ValueError("q must be [batch][q_len][num_q_heads][head_dim]")
+    _dev(seq_lens, "seq_lens", torch.int32, 1)
+    _dev(full_block_table, "full_block_table", torch.int32, 2)
+    if seq_lens.shape[0] != B or full_block_table.shape[0] != B:
+        raise ValueError("seq_lens / full_block_table must have batch rows")
+    out, lse = _outputs((B, q_len, kv.num_q_heads, kv.head_dim), q.device, out, lse)
+    need = verify_workspace_bytes(kv, B, q_len, max_seq_len, num_splits)
+    workspace, have = _workspace(need, q.device, workspace)
+    st = lib.kap_verify(
+        ctypes.byref(kv.struct), B, q_len, _ptr(q), _ptr(seq_lens), _ptr(full_block_table),
+        full_block_table.shape[1], int(max_seq_len), float(sm_scale), int(num_splits),
+        _ptr(out), _ptr(lse), _ptr(workspace), have, _stream(stream))
+    _check(st)
+    return out, lse
+
+
+def abi_version() -> int:
+    return int(load_library().kap_abi_version())

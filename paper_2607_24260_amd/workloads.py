@@ -218,9 +218,11 @@ DESCRIPTIONS = {
 def make_workload(config: int, device="cpu", replicas: int = 1, batch: Optional[int] = None,
                   seq_len: Optional[int] = None, seed: Optional[int] = None,
                   n_decode: Optional[int] = None, n_verify: Optional[int] = None,
-                  num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128) -> Workload:
+                  num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128,
+                  with_kv: bool = True) -> Workload:
     """Build workload ``config`` (1..5). ``batch`` / ``seq_len`` / step counts may
-    be shrunk for tests; the recipe is otherwise unchanged."""
+    be shrunk for tests; the recipe is otherwise unchanged. ``with_kv=False``
+    skips drawing the KV pools (plan-only use)."""
     seed = config_seed(config) if seed is None else seed
     rng = np.random.Generator(np.random.PCG64(seed))
     Hq, Hkv, D = num_q_heads, num_kv_heads, head_dim
@@ -303,7 +305,7 @@ def make_workload(config: int, device="cpu", replicas: int = 1, batch: Optional[
     offs, st, ln, pr = _csr(per)
 
     ks, vs, scs = [], [], []
-    for r in range(replicas):
+    for r in range(replicas if with_kv else 0):
         k, v, sc = kv_pool(num_pages, Hkv, D, kv_dtype, seed + 17 + 7919 * r, device)
         ks.append(k); vs.append(v); scs.append(sc)
 

@@ -1,0 +1,143 @@
+"""C-ABI checks that need no GPU: libkap.so loads, exports every function that
+include/kap.h declares, and host-side validation rejects bad arguments before
+anything is enqueued (fake pointers are never dereferenced on those paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_24260_amd import kap as K
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kap.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(K.LIB_PATH):
+        pytest.fail("libkap.so is not built; run __graft_entry__.build() first")
+    return K.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kap_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("kap_compile_plan", "kap_selected_decode", "kap_verify"):
+        assert n in names
+    assert set(names) == set(K.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_version_and_status_strings(lib):
+    assert lib.kap_abi_version() == 1
+    assert lib.kap_status_string(0) == b"KAP_OK"
+    assert lib.kap_status_string(3) == b"KAP_ERR_WORKSPACE_TOO_SMALL"
+    assert lib.kap_status_string(99) == b"KAP_UNKNOWN_STATUS"
+
+
+FAKE = 0x10000        # aligned, never dereferenced on the rejected paths
+
+
+def kv_struct(kv_dtype=K.KAP_DT_BF16, q_dtype=K.KAP_DT_BF16, Hq=32, Hkv=8, D=128, page=16,
+              scales=None, num_pages=100):
+    return K.KVCacheStruct(Hq, Hkv, D, page, kv_dtype, q_dtype, FAKE, FAKE, scales, num_pages)
+
+
+def decode_call(lib, kv, batch=2, q_len_unused=None, view_stride=8, max_view_blocks=8,
+                num_splits=0, ws=None, ws_bytes=0, sm_scale=1.0, q=FAKE):
+    return lib.kap_selected_decode(ctypes.byref(kv), batch, q, FAKE, FAKE, FAKE, view_stride,
+                                   FAKE, max_view_blocks, sm_scale, num_splits, FAKE, FAKE,
+                                   ws, ws_bytes, None)
+
+
+def verify_call(lib, kv, batch=2, q_len=5, fbt_stride=8, max_seq_len=128, ws=None, ws_bytes=0):
+    return lib.kap_verify(ctypes.byref(kv), batch, q_len, FAKE, FAKE, FAKE, fbt_stride,
+                          max_seq_len, 1.0, 0, FAKE, FAKE, ws, ws_bytes, None)
+
+
+def test_decode_rejects_bad_geometry(lib):
+    assert decode_call(lib, kv_struct(page=32)) == K.KAP_ERR_UNSUPPORTED
+    assert decode_call(lib, kv_struct(D=96)) == K.KAP_ERR_UNSUPPORTED
+    assert decode_call(lib, kv_struct(Hq=30, Hkv=8)) == K.KAP_ERR_INVALID_ARGUMENT
+    assert decode_call(lib, kv_struct(kv_dtype=K.KAP_DT_F32)) == K.KAP_ERR_UNSUPPORTED
+    assert decode_call(lib, kv_struct(kv_dtype=K.KAP_DT_FP8_E4M3FN)) == K.KAP_ERR_INVALID_ARGUMENT
+    assert b"kv_scales" in lib.kap_last_error()
+    assert decode_call(lib, kv_struct(), batch=-1) == K.KAP_ERR_INVALID_ARGUMENT
+    assert decode_call(lib, kv_struct(), max_view_blocks=9) == K.KAP_ERR_INVALID_ARGUMENT
+    assert decode_call(lib, kv_struct(), num_splits=-2) == K.KAP_ERR_INVALID_ARGUMENT
+    assert decode_call(lib, kv_struct(), sm_scale=float("nan")) == K.KAP_ERR_INVALID_ARGUMENT
+    assert decode_call(lib, kv_struct(), q=FAKE + 4) == K.KAP_ERR_INVALID_ARGUMENT
+    assert decode_call(lib, None if False else kv_struct(), batch=70000) == K.KAP_ERR_UNSUPPORTED
+
+
+def test_zero_batch_is_a_noop(lib):
+    assert decode_call(lib, kv_struct(), batch=0) == K.KAP_OK
+    assert verify_call(lib, kv_struct(), batch=0) == K.KAP_OK
+    assert lib.kap_last_error() == b""
+
+
+def test_verify_rejects_bad_window(lib):
+    assert verify_call(lib, kv_struct(), q_len=0) == K.KAP_ERR_INVALID_ARGUMENT
+    assert verify_call(lib, kv_struct(), q_len=17) == K.KAP_ERR_INVALID_ARGUMENT
+    assert verify_call(lib, kv_struct(), fbt_stride=7, max_seq_len=128) == K.KAP_ERR_INVALID_ARGUMENT
+    assert verify_call(lib, kv_struct(), max_seq_len=-1) == K.KAP_ERR_INVALID_ARGUMENT
+
+
+def test_workspace_too_small_is_reported_before_launch(lib):
+    kv = kv_struct()
+    need = lib.kap_verify_workspace_bytes(ctypes.byref(kv), 4, 5, 131072, 0)
+    assert need > 0
+    assert verify_call(lib, kv, batch=4, fbt_stride=8192, max_seq_len=131072,
+                       ws=FAKE, ws_bytes=need - 1) == K.KAP_ERR_WORKSPACE_TOO_SMALL
+    need_d = lib.kap_selected_decode_workspace_bytes(ctypes.byref(kv), 4, 451, 0)
+    assert need_d > 0
+    assert decode_call(lib, kv, batch=4, view_stride=451, max_view_blocks=451,
+                       ws=FAKE, ws_bytes=need_d - 1) == K.KAP_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_workspace_sizes_are_monotone(lib):
+    kv = kv_struct()
+    prev = 0
+    for L in (16, 1024, 16384, 131072):
+        need = lib.kap_verify_workspace_bytes(ctypes.byref(kv), 4, 5, L, 64)
+        assert need >= prev
+        prev = need
+    # one forced split needs no partials
+    assert lib.kap_verify_workspace_bytes(ctypes.byref(kv), 4, 5, 131072, 1) == 0
+    assert lib.kap_selected_decode_workspace_bytes(ctypes.byref(kv), 4, 451, 1) == 0
+
+
+def plan_call(lib, batch=1, fbt_stride=8, num_spans=4, policy=0, cap=8, ws=None, ws_bytes=0):
+    return lib.kap_compile_plan(batch, FAKE, FAKE, fbt_stride, FAKE, num_spans, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, FAKE, policy, 100, cap, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                FAKE, None, ws, ws_bytes, None)
+
+
+def test_compile_plan_rejects_bad_arguments(lib):
+    assert plan_call(lib, batch=-1) == K.KAP_ERR_INVALID_ARGUMENT
+    assert plan_call(lib, policy=7) == K.KAP_ERR_INVALID_ARGUMENT
+    assert plan_call(lib, fbt_stride=0) == K.KAP_ERR_INVALID_ARGUMENT
+    assert plan_call(lib, fbt_stride=262145) == K.KAP_ERR_UNSUPPORTED
+    assert plan_call(lib, cap=-1) == K.KAP_ERR_INVALID_ARGUMENT
+    assert plan_call(lib, num_spans=4, ws=None) == K.KAP_ERR_WORKSPACE_TOO_SMALL
+    assert plan_call(lib, batch=0) == K.KAP_OK
+    assert lib.kap_compile_plan_workspace_bytes(1, 4, 8) == 256
+    assert lib.kap_compile_plan_workspace_bytes(1, 0, 8) == 0
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    with pytest.raises(ValueError, match="GPU tensor"):
+        K.KVCache(torch.zeros(2, 1, 16, 128, dtype=torch.bfloat16),
+                  torch.zeros(2, 1, 128, 16, dtype=torch.bfloat16), 4, torch.bfloat16)

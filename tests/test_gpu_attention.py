@@ -1,0 +1,294 @@
+"""GPU parity of kap_selected_decode and kap_verify against the fp64 oracle.
+
+Tolerances (bf16 / fp8 / fp32 inputs, fp32 outputs): max |O - O_ref| <= 2e-3,
+max |LSE - LSE_ref| <= 1e-3, both sides reading the same stored KV bits.
+Small and mid-size workloads are checked on every step; the 128K workload and
+the 64-sequence fp8 workload on seeded subsets of steps / sequences / KV heads
+(the subsets are named in each test), in the launch configuration bench.py
+times.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import kap_oracle as O
+from paper_2607_24260_amd import kap as K
+from paper_2607_24260_amd.workloads import make_workload
+
+from kap_testlib import (LSE_TOL, O_TOL, assert_close, dev_i32, full_view, gpu_plan, kv_of,
+                         oracle_plan, oracle_pool, plan_view_arrays)
+
+pytestmark = pytest.mark.gpu
+
+_CACHE = {}
+
+
+def workload(config, **kw):
+    key = (config, tuple(sorted(kw.items())))
+    if key not in _CACHE:
+        _CACHE.clear()
+        torch.cuda.empty_cache()
+        w = make_workload(config, device="cuda", **kw)
+        _CACHE[key] = (w, oracle_pool(w))
+    return _CACHE[key]
+
+
+def decode_check(w, pool, steps, budget=None, num_splits=0, batches=None):
+    plan = gpu_plan(w, budget=budget)
+    plans = oracle_plan(w, budget=budget)
+    cap = w.max_pages_per_seq
+    vbt, vlb, nb = plan_view_arrays(plans, cap)
+    kv = kv_of(w)
+    worst = [0.0, 0.0]
+    for s in steps:
+        q = w.q_decode[s]
+        o, lse = K.selected_decode(kv, q, dev_i32(w.seq_lens), plan["view_block_table"],
+                                   plan["view_logical_block"], plan["view_num_blocks"], cap,
+                                   w.sm_scale, num_splits=num_splits)
+        torch.cuda.synchronize()
+        qh = q.float().cpu().numpy()
+        sel = list(range(w.batch)) if batches is None else batches
+        eo, el = O.selected_decode(pool, qh[sel], w.seq_lens[sel], vbt[sel], vlb[sel], nb[sel],
+                                   w.sm_scale)
+        worst[0] = max(worst[0], assert_close(f"O step {s}", o.cpu().numpy()[sel], eo, O_TOL))
+        worst[1] = max(worst[1], assert_close(f"LSE step {s}", lse.cpu().numpy()[sel], el,
+                                              LSE_TOL))
+    return worst
+
+
+def verify_check(w, pool, calls, num_splits=0, batches=None, kv_heads=None):
+    kv = kv_of(w)
+    Hkv, G = w.num_kv_heads, w.num_q_heads // w.num_kv_heads
+    for c in calls:
+        q = w.q_verify[c]
+        o, lse = K.verify(kv, q, dev_i32(w.seq_lens), dev_i32(w.full_block_table),
+                          int(w.seq_lens.max()), w.sm_scale, num_splits=num_splits)
+        torch.cuda.synchronize()
+        eo, el = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, w.full_block_table,
+                          w.sm_scale, batches=batches, kv_heads=kv_heads)
+        bs = list(range(w.batch)) if batches is None else batches
+        hs = list(range(Hkv)) if kv_heads is None else kv_heads
+        heads = [g * G + j for g in hs for j in range(G)]
+        on, ln = o.cpu().numpy(), lse.cpu().numpy()
+        assert_close(f"verify O call {c}", on[np.ix_(bs, range(q.shape[1]), heads)],
+                     eo[np.ix_(bs, range(q.shape[1]), heads)], O_TOL)
+        assert_close(f"verify LSE call {c}", ln[np.ix_(bs, range(q.shape[1]), heads)],
+                     el[np.ix_(bs, range(q.shape[1]), heads)], LSE_TOL)
+
+
+# --------------------------------------------------------------------------
+# the five workloads
+# --------------------------------------------------------------------------
+
+def test_config1_fp32():
+    w, pool = workload(1)
+    decode_check(w, pool, [0])
+    verify_check(w, pool, [0])
+
+
+def test_config2_decode_all_steps():
+    w, pool = workload(2)
+    decode_check(w, pool, range(32))
+
+
+def test_config2_verify_all_calls():
+    w, pool = workload(2)
+    verify_check(w, pool, range(8))
+
+
+@pytest.mark.parametrize("first", [0, 8, 16, 24])
+def test_config3_decode_all_steps(first):
+    w, pool = workload(3)
+    decode_check(w, pool, range(first, first + 8))
+
+
+def test_config3_all_blocks_plan_equals_full_decode():
+    """The all-blocks plan (the full block table as the view, what fallback
+    uses) must equal full decode: checked against the oracle, against verify
+    with a one-token window, and built by the plan kernel from a span that
+    covers the whole sequence."""
+    w, pool = workload(3)
+    kv = kv_of(w)
+    fbt, lblk, npg, mx = full_view(w)
+    full_b = np.asarray(w.full_block_table, dtype=np.int64)
+    full_l = np.tile(np.arange(w.fbt_stride), (w.batch, 1))
+    for s in (0, 31):
+        q = w.q_decode[s]
+        o, lse = K.selected_decode(kv, q, dev_i32(w.seq_lens), fbt, lblk, npg, mx, 1.0)
+        ov, lv = K.verify(kv, q[:, None].contiguous(), dev_i32(w.seq_lens), fbt, mx * 16, 1.0)
+        torch.cuda.synchronize()
+        eo, el = O.selected_decode(pool, q.float().cpu().numpy(), w.seq_lens, full_b, full_l,
+                                   npg.cpu().numpy(), 1.0)
+        assert_close("full-view O", o.cpu().numpy(), eo, O_TOL)
+        assert_close("full-view LSE", lse.cpu().numpy(), el, LSE_TOL)
+        assert (o - ov[:, 0]).abs().max().item() <= O_TOL
+        assert (lse - lv[:, 0]).abs().max().item() <= LSE_TOL
+    # budget = L plus one span over [0, L): the plan kernel emits the full table
+    B = w.batch
+    offs = np.arange(B + 1, dtype=np.int32)
+    plan = K.compile_plan(dev_i32(w.seq_lens), fbt, dev_i32(offs), dev_i32(np.zeros(B)),
+                          dev_i32(w.seq_lens), torch.ones(B, device="cuda"),
+                          dev_i32(w.prefix), dev_i32(w.suffix), dev_i32(w.seq_lens),
+                          num_pages=w.num_pages, view_capacity=w.fbt_stride)
+    torch.cuda.synchronize()
+    assert torch.equal(plan["view_block_table"], fbt)
+    assert torch.equal(plan["view_num_blocks"], npg)
+    assert torch.equal(plan["view_tokens"], dev_i32(w.seq_lens))
+
+
+def test_config3_verify():
+    w, pool = workload(3)
+    verify_check(w, pool, [0, 7], batches=[0, 5, 15])
+
+
+def test_config4_decode_sampled_steps():
+    # steps 0, 21, 42, 63 of 64, every sequence and head
+    w, pool = workload(4, n_verify=2)
+    decode_check(w, pool, [0, 21, 42, 63])
+
+
+def test_config4_verify_sampled():
+    # verify call 0 and 1; sequences {0, 3} x KV heads {0, 7}
+    w, pool = workload(4, n_verify=2)
+    verify_check(w, pool, [0, 1], batches=[0, 3], kv_heads=[0, 7])
+
+
+def test_config5_fp8_decode():
+    # decode steps 0 and last, all 64 ragged sequences on the GPU; the oracle
+    # checks every fourth sequence (0, 4, ..., 60)
+    w, pool = workload(5)
+    decode_check(w, pool, [0, w.q_decode.shape[0] - 1], batches=list(range(0, 64, 4)))
+
+
+def test_config5_fp8_verify_each_window_size():
+    # one verify call per distinct gamma; sequences 0, 17, 63 x KV heads 0, 5
+    w, pool = workload(5)
+    gammas = [q.shape[1] - 1 for q in w.q_verify]
+    first = {g: c for c, g in reversed(list(enumerate(gammas)))}
+    verify_check(w, pool, sorted(first.values()), batches=[0, 17, 63], kv_heads=[0, 5])
+
+
+# --------------------------------------------------------------------------
+# cross-checks and edge cases on small shapes (several tiles + ragged tails)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_split_count_does_not_change_result(kv_dtype):
+    cfg = 2 if kv_dtype == "bf16" else 5
+    kw = dict(batch=3, seq_len=5000, n_decode=1, n_verify=1)
+    w, pool = workload(cfg, **kw)
+    for ns in (1, 3, 10_000):
+        decode_check(w, pool, [0], num_splits=ns)
+        verify_check(w, pool, [0], num_splits=ns)
+
+
+def test_view_order_does_not_matter():
+    w, pool = workload(2, batch=2, seq_len=4000, n_decode=1, n_verify=1)
+    plan = gpu_plan(w)
+    kv = kv_of(w)
+    args = (dev_i32(w.seq_lens),)
+    o1, l1 = K.selected_decode(kv, w.q_decode[0], *args, plan["view_block_table"],
+                               plan["view_logical_block"], plan["view_num_blocks"],
+                               w.max_pages_per_seq, 1.0)
+    vbt = plan["view_block_table"].clone()
+    vlb = plan["view_logical_block"].clone()
+    g = torch.Generator(device="cpu").manual_seed(3)
+    for b in range(w.batch):
+        n = int(plan["view_num_blocks"][b])
+        perm = torch.randperm(n, generator=g).cuda()
+        vbt[b, :n] = vbt[b, :n][perm]
+        vlb[b, :n] = vlb[b, :n][perm]
+    o2, l2 = K.selected_decode(kv, w.q_decode[0], *args, vbt, vlb, plan["view_num_blocks"],
+                               w.max_pages_per_seq, 1.0)
+    torch.cuda.synchronize()
+    assert (o1 - o2).abs().max().item() <= 1e-5
+    assert (l1 - l2).abs().max().item() <= 1e-5
+
+
+def test_verify_one_token_equals_all_blocks_decode():
+    w, pool = workload(2, batch=3, seq_len=3000, n_decode=1, n_verify=1)
+    kv = kv_of(w)
+    fbt, lblk, npg, mx = full_view(w)
+    q = w.q_decode[0]
+    od, ld = K.selected_decode(kv, q, dev_i32(w.seq_lens), fbt, lblk, npg, mx, 1.0)
+    ov, lv = K.verify(kv, q[:, None].contiguous(), dev_i32(w.seq_lens), fbt, mx * 16, 1.0)
+    torch.cuda.synchronize()
+    assert (od - ov[:, 0]).abs().max().item() <= 2e-3
+    assert (ld - lv[:, 0]).abs().max().item() <= 1e-3
+
+
+@pytest.mark.parametrize("q_len", [1, 2, 3, 4, 5, 8, 9, 13, 16])
+def test_verify_window_sizes_ragged(q_len):
+    # ragged lengths (not multiples of 16), windows from 1 to 16 query tokens
+    w, pool = workload(2, batch=4, seq_len=1000, n_decode=1, n_verify=1)
+    w.seq_lens[:] = [1000, 999, 37, q_len]
+    g = torch.Generator(device="cuda").manual_seed(q_len)
+    q = (torch.randn((4, q_len, 32, 128), generator=g, device="cuda") / 11.3).to(torch.bfloat16)
+    kv = kv_of(w)
+    o, lse = K.verify(kv, q, dev_i32(w.seq_lens), dev_i32(w.full_block_table), 1000, 1.0)
+    torch.cuda.synchronize()
+    eo, el = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, w.full_block_table, 1.0)
+    assert_close("O", o.cpu().numpy(), eo, O_TOL)
+    assert_close("LSE", lse.cpu().numpy(), el, LSE_TOL)
+
+
+def test_window_longer_than_sequence_gives_empty_rows():
+    w, pool = workload(2, batch=2, seq_len=100, n_decode=1, n_verify=1)
+    w.seq_lens[:] = [3, 100]
+    q = w.q_verify[0]                                      # q_len 5 > L = 3 for sequence 0
+    o, lse = K.verify(kv_of(w), q, dev_i32(w.seq_lens), dev_i32(w.full_block_table), 100, 1.0)
+    torch.cuda.synchronize()
+    eo, el = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, w.full_block_table, 1.0)
+    assert np.all(np.isneginf(lse.cpu().numpy()[0, :2]))
+    assert np.all(o.cpu().numpy()[0, :2] == 0)
+    assert_close("O", o.cpu().numpy(), eo, O_TOL)
+    assert_close("LSE", lse.cpu().numpy(), el, LSE_TOL)
+
+
+def test_empty_view_gives_zero_and_neg_inf():
+    w, _ = workload(2, batch=2, seq_len=500, n_decode=1, n_verify=1)
+    plan = gpu_plan(w)
+    nb = plan["view_num_blocks"].clone()
+    nb[1] = 0
+    o, lse = K.selected_decode(kv_of(w), w.q_decode[0], dev_i32(w.seq_lens),
+                               plan["view_block_table"], plan["view_logical_block"], nb,
+                               w.max_pages_per_seq, 1.0)
+    torch.cuda.synchronize()
+    assert torch.all(o[1] == 0) and torch.all(torch.isneginf(lse[1]))
+    assert torch.all(torch.isfinite(lse[0]))
+
+
+@pytest.mark.parametrize("alpha", [8.0, 16.0])
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_peaky_planted_keys(alpha, kv_dtype):
+    """Plant K_t = alpha q_h / |q_h|^2 (then stored in the KV dtype) at a few
+    selected positions so one logit per head dominates: stresses the max
+    subtraction, the split merge and the rounding of P."""
+    cfg = 2 if kv_dtype == "bf16" else 5
+    w, _ = workload(cfg, batch=2, seq_len=6000, n_decode=1, n_verify=1)
+    plans = oracle_plan(w)
+    rng = np.random.default_rng(int(alpha))
+    k = w.k_pages[0]
+    q = w.q_decode[0].float()
+    for b, p in enumerate(plans):
+        for _ in range(3):
+            kk = int(rng.integers(0, p.num_blocks))
+            page, lb = p.block_table[kk], p.logical_blocks[kk]
+            slot = int(rng.integers(0, min(16, int(w.seq_lens[b]) - 16 * lb)))
+            for g in range(w.num_kv_heads):
+                h = g * 4 + int(rng.integers(0, 4))
+                vec = alpha * q[b, h] / (q[b, h] @ q[b, h])
+                if kv_dtype == "bf16":
+                    k[page, g, slot] = vec.to(torch.bfloat16)
+                else:
+                    sc = float(w.kv_scales[0][page, 0])
+                    k[page, g, slot] = (vec / sc).clamp(-448, 448).to(
+                        torch.float8_e4m3fn).view(torch.uint8)
+    pool = oracle_pool(w)
+    _CACHE.clear()
+    decode_check(w, pool, [0])
+    decode_check(w, pool, [0], num_splits=1)
+    # the planted keys also sit in the full KV the verify window reads
+    qv = w.q_decode[0][:, None].repeat(1, 3, 1, 1).contiguous()
+    w.q_verify = [qv]
+    verify_check(w, pool, [0])
