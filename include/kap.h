@@ -26,7 +26,14 @@
  *   until that work has completed.
  * - Scratch memory comes from the caller's `workspace`, at least the size the
  *   matching kap_*_workspace_bytes() call returns for the same arguments on
- *   the current device. Its contents on entry do not matter.
+ *   the current device, 256-byte aligned. kap_selected_decode and kap_verify
+ *   keep arrival counters in its first round_up(4 * batch * num_kv_heads, 256)
+ *   bytes: that block must be zero when the call starts, and every completed
+ *   call leaves it zero again. Zero-fill a workspace once when allocating it
+ *   (and again if a later call uses a larger batch * num_kv_heads); the rest
+ *   of the workspace is scratch whose contents do not matter. Calls that can
+ *   run concurrently must not share a workspace. kap_compile_plan's workspace
+ *   has no such block.
  * - Grid sizes depend only on host integers, never on device data, so the
  *   calls may be captured into a HIP graph.
  * - Host-checkable errors (null pointers, negative sizes, unsupported

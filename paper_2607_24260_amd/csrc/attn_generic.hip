@@ -43,8 +43,9 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(AttnArgs a) {
   int nb = a.num_blocks ? a.num_blocks[b] : np_seq;
   nb = max(0, min(nb, a.max_blocks));
   const int limit = a.causal ? (L - a.q_len + i + 1) : L;   // visible positions < limit
-  const int k0 = split * a.pages_per_split;
-  const int k1 = min(nb, k0 + a.pages_per_split);
+  // split `split` of n_split takes an even share (<= pages_per_split pages)
+  const int k0 = (int)(((long long)split * nb) / a.n_split);
+  const int k1 = (int)(((long long)(split + 1) * nb) / a.n_split);
   const size_t row = (size_t)b * R + r;
   float *po = (a.n_split == 1) ? a.out + row * D : a.part_o + (row * a.n_split + split) * D;
 

@@ -2,9 +2,13 @@
 // query heads per KV head -- the proposal step of Sec. 3.2 of the paper.
 //
 // Work decomposition: one 256-thread workgroup per (key split, KV head,
-// sequence). Its four wavefronts take the split's view pages round-robin, keep
-// their own online-softmax state, and merge through LDS at the end. With more
-// than one split the result is a partial (o, lse) that merge.hip combines.
+// sequence); split s of n takes view pages [s*nb/n, (s+1)*nb/n) of the
+// sequence's actual view length nb. Its four wavefronts take those pages
+// round-robin (the next page's loads in flight while one is processed), keep
+// their own online-softmax state, and merge through LDS at the end. With more than one
+// split the workgroup writes a partial (o, lse); the workgroup that finishes
+// last for its (sequence, KV head) merges all splits (atomic arrival counter
+// in the workspace), so one launch produces the final output.
 //
 // Per page (16 tokens x 128 dims = 4 KB of bf16 K and 4 KB of V^T):
 //  * K phase: lane (t = lane/4, c = lane%4) loads dims {32i + 8c .. +7}, i<4,
@@ -152,6 +156,9 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   __shared__ float pbuf[kWaves][64];
   __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
   __shared__ float wacc[kWaves][4][kD];
+  __shared__ float s_part[4][kD];
+  __shared__ float s_plse[4];
+  __shared__ int s_flag;
 
   const int split = blockIdx.x;
   const int g = blockIdx.y;
@@ -163,8 +170,9 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   const int L = a.seq_lens[b];
   int nb = a.num_blocks[b];
   nb = max(0, min(nb, a.max_blocks));
-  const int k0 = split * a.pages_per_split;
-  const int k1 = min(nb, k0 + a.pages_per_split);
+  // split `split` of n_split takes an even share of this sequence's view
+  const int k0 = (int)(((long long)split * nb) / a.n_split);
+  const int k1 = (int)(((long long)(split + 1) * nb) / a.n_split);
   const int32_t *vbt = a.block_table + (size_t)b * a.bt_stride;
   const int32_t *vlb = a.logical_block + (size_t)b * a.bt_stride;
 
@@ -190,113 +198,124 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[hh][i] = 0.f;
 
-  auto page_info = [&](int k, int &page, int &nvalid) {
-    page = vbt[k];
-    const long long rem = (long long)L - (long long)vlb[k] * kPage;
+  // View block kk of this wavefront -> a page that is safe to read (page 0
+  // stands in for an invalid id) and its number of visible tokens (0 if the
+  // id is invalid or the block lies past the sequence).
+  auto page_info = [&](int kk, int &page, int &nvalid) {
+    page = vbt[kk];
+    const long long rem = (long long)L - (long long)vlb[kk] * kPage;
     nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
-    if (page < 0 || (int64_t)page >= a.num_pages) nvalid = 0;
+    if (page < 0 || (int64_t)page >= a.num_pages) {
+      nvalid = 0;
+      page = 0;
+    }
   };
 
-  int k = k0 + wave;
-  int page = 0, nvalid = 0;
-  PageRegs<KV> cur;
-  if (k < k1) {
-    page_info(k, page, nvalid);
-    if (nvalid > 0) load_page<KV>(cur, a, page, g, lane);
-  }
-  while (k < k1) {
-    const int kn = k + kWaves;
-    int npage = 0, nnvalid = 0;
-    PageRegs<KV> nxt;
-    if (kn < k1) {
-      page_info(kn, npage, nnvalid);
-      if (nnvalid > 0) load_page<KV>(nxt, a, npage, g, lane);
+  auto process = [&](const PageRegs<KV> &cur, int page, int nvalid) {
+    float ksc = a.scale_log2, vsc = 1.f;
+    if constexpr (KV == kFP8) {
+      ksc *= a.kv_scales[2 * (size_t)page];
+      vsc = a.kv_scales[2 * (size_t)page + 1];
     }
-    if (nvalid > 0) {
-      float ksc = a.scale_log2, vsc = 1.f;
-      if constexpr (KV == kFP8) {
-        ksc *= a.kv_scales[2 * (size_t)page];
-        vsc = a.kv_scales[2 * (size_t)page + 1];
+    // ---- logits --------------------------------------------------------------
+    uint32_t kk[4][4];
+    k_pairs<KV>(cur, kk);
+    float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        d0 = dot2(kk[i][w], qr[0][i][w], d0);
+        d1 = dot2(kk[i][w], qr[1][i][w], d1);
+        d2 = dot2(kk[i][w], qr[2][i][w], d2);
+        d3 = dot2(kk[i][w], qr[3][i][w], d3);
       }
-      // ---- logits ------------------------------------------------------------
-      uint32_t kk[4][4];
-      k_pairs<KV>(cur, kk);
-      float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          d0 = dot2(kk[i][w], qr[0][i][w], d0);
-          d1 = dot2(kk[i][w], qr[1][i][w], d1);
-          d2 = dot2(kk[i][w], qr[2][i][w], d2);
-          d3 = dot2(kk[i][w], qr[3][i][w], d3);
-        }
-      // transposing reduction inside the quad: lane c ends with head c
-      const bool o1 = c & 1, o2 = c & 2;
-      float keep0 = o1 ? d1 : d0, send0 = o1 ? d0 : d1;
-      float keep1 = o1 ? d3 : d2, send1 = o1 ? d2 : d3;
-      keep0 += dpp<kQuadXor1>(send0);
-      keep1 += dpp<kQuadXor1>(send1);
-      float s = o2 ? keep1 : keep0;
-      s += dpp<kQuadXor2>(o2 ? keep0 : keep1);
-      s = (t < nvalid) ? s * ksc : -INFINITY;
+    // transposing reduction inside the quad: lane c ends with head c
+    const bool o1 = c & 1, o2 = c & 2;
+    float keep0 = o1 ? d1 : d0, send0 = o1 ? d0 : d1;
+    float keep1 = o1 ? d3 : d2, send1 = o1 ? d2 : d3;
+    keep0 += dpp<kQuadXor1>(send0);
+    keep1 += dpp<kQuadXor1>(send1);
+    float s = o2 ? keep1 : keep0;
+    s += dpp<kQuadXor2>(o2 ? keep0 : keep1);
+    s = (t < nvalid) ? s * ksc : -INFINITY;
 
-      // ---- online softmax --------------------------------------------------
-      float pm = fmaxf(s, dpp<kRowRor4>(s));
-      pm = fmaxf(pm, dpp<kRowRor8>(pm));
-      pm = xor16_max(pm);
-      pm = xor32_max(pm);
-      const float m_new = fmaxf(m_c, pm);
-      if (__any(m_new > m_c)) {
-        const float alpha = exp2f(m_c - (m_new == -INFINITY ? 0.f : m_new));
-        l_c *= alpha;
-        float al[4];
+    // ---- online softmax ------------------------------------------------------
+    float pm = fmaxf(s, dpp<kRowRor4>(s));
+    pm = fmaxf(pm, dpp<kRowRor8>(pm));
+    pm = xor16_max(pm);
+    pm = xor32_max(pm);
+    const float m_new = fmaxf(m_c, pm);
+    if (__any(m_new > m_c)) {
+      const float alpha = exp2f(m_c - (m_new == -INFINITY ? 0.f : m_new));
+      l_c *= alpha;
+      float al[4];
 #pragma unroll
-        for (int hh = 0; hh < 4; ++hh)
-          al[hh] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), hh));
+      for (int hh = 0; hh < 4; ++hh)
+        al[hh] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), hh));
 #pragma unroll
-        for (int hh = 0; hh < 4; ++hh)
+      for (int hh = 0; hh < 4; ++hh)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc[hh][i] *= al[hh];
-        m_c = m_new;
-      }
-      const float p = exp2f(s - (m_c == -INFINITY ? 0.f : m_c));
-      l_c += p;
-      pbuf[wave][lane] = p * vsc;
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        for (int i = 0; i < 4; ++i) acc[hh][i] *= al[hh];
+      m_c = m_new;
+    }
+    const float p = exp2f(s - (m_c == -INFINITY ? 0.f : m_c));
+    l_c += p;
+    pbuf[wave][lane] = p * vsc;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-      // ---- o += p V ----------------------------------------------------------
-      float vv[4][8];
-      v_floats<KV>(cur, vv);
-      if (nvalid < kPage) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const bool ok = hf * 8 + j < nvalid;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) vv[i][j] = ok ? vv[i][j] : 0.f;
-        }
-      }
+    // ---- o += p V --------------------------------------------------------------
+    float vv[4][8];
+    v_floats<KV>(cur, vv);
+    if (nvalid < kPage) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float4 pj = *reinterpret_cast<const float4 *>(&pbuf[wave][(hf * 8 + j) * 4]);
+        const bool ok = hf * 8 + j < nvalid;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc[0][i] = fmaf(pj.x, vv[i][j], acc[0][i]);
-          acc[1][i] = fmaf(pj.y, vv[i][j], acc[1][i]);
-          acc[2][i] = fmaf(pj.z, vv[i][j], acc[2][i]);
-          acc[3][i] = fmaf(pj.w, vv[i][j], acc[3][i]);
-        }
+        for (int i = 0; i < 4; ++i) vv[i][j] = ok ? vv[i][j] : 0.f;
       }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    k = kn;
-    page = npage;
-    nvalid = nnvalid;
-    cur = nxt;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float4 pj = *reinterpret_cast<const float4 *>(&pbuf[wave][(hf * 8 + j) * 4]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[0][i] = fmaf(pj.x, vv[i][j], acc[0][i]);
+        acc[1][i] = fmaf(pj.y, vv[i][j], acc[1][i]);
+        acc[2][i] = fmaf(pj.z, vv[i][j], acc[2][i]);
+        acc[3][i] = fmaf(pj.w, vv[i][j], acc[3][i]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  // Two page buffers, unrolled by two: while one page is processed the loads of
+  // the next are in flight. Loads are unconditional (past the end of this
+  // wavefront's pages the last page is re-read, an L2 hit) so the steady state
+  // is straight-line code and only the older buffer's loads are waited for.
+  const int kw = k0 + wave;
+  const int n_my = kw < k1 ? (k1 - kw + kWaves - 1) / kWaves : 0;
+  if (n_my > 0) {
+    auto kidx = [&](int i) { return kw + kWaves * min(i, n_my - 1); };
+    PageRegs<KV> ra, rb;
+    int pga, nva, pgb, nvb;
+    page_info(kidx(0), pga, nva);
+    load_page<KV>(ra, a, pga, g, lane);
+    page_info(kidx(1), pgb, nvb);
+    load_page<KV>(rb, a, pgb, g, lane);
+    for (int i = 0; i < n_my; i += 2) {
+      process(ra, pga, nva);
+      page_info(kidx(i + 2), pga, nva);
+      load_page<KV>(ra, a, pga, g, lane);
+      if (i + 1 >= n_my) break;
+      process(rb, pgb, nvb);
+      page_info(kidx(i + 3), pgb, nvb);
+      load_page<KV>(rb, a, pgb, g, lane);
+    }
   }
 
   // ---- per-wave totals -------------------------------------------------------
@@ -344,11 +363,28 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   if (a.n_split == 1) {
     *reinterpret_cast<float2 *>(a.out + row * kD + d0) = make_float2(o0, o1v);
     if ((threadIdx.x & 63) == 0) a.lse[row] = lse2 * kLn2;
-  } else {
-    const size_t pr = row * a.n_split + split;
-    *reinterpret_cast<float2 *>(a.part_o + pr * kD + d0) = make_float2(o0, o1v);
-    if ((threadIdx.x & 63) == 0) a.part_lse[pr] = lse2;
+    return;
   }
+  // several splits: stage the partial in LDS, wavefront 0 writes it and takes
+  // the arrival ticket; the last workgroup of (b, g) merges the splits
+  *reinterpret_cast<float2 *>(&s_part[hh][d0]) = make_float2(o0, o1v);
+  if ((threadIdx.x & 63) == 0) s_plse[hh] = lse2;
+  __syncthreads();
+  if (threadIdx.x < 64) {
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const int f = threadIdx.x + 64 * t2;       // float4 index in [4][128]
+      const int h4 = f >> 5, d4 = (f & 31) * 4;
+      const size_t pr = ((size_t)b * a.Hq + g * 4 + h4) * a.n_split + split;
+      *reinterpret_cast<float4 *>(a.part_o + pr * kD + d4) =
+          *reinterpret_cast<const float4 *>(&s_part[h4][d4]);
+    }
+    if (threadIdx.x < 4) {
+      const size_t pr = ((size_t)b * a.Hq + g * 4 + threadIdx.x) * a.n_split + split;
+      a.part_lse[pr] = s_plse[threadIdx.x];
+    }
+  }
+  if (last_arrival(a, b, g, &s_flag)) merge_rows(a, b, g, 4);
 }
 
 }  // namespace
@@ -362,6 +398,15 @@ hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s) {
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+int decode_fast_blocks_per_cu(int kv_type) {
+  int nb = 0;
+  const hipError_t e =
+      kv_type == kFP8
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kFP8>, 256, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kBF16>, 256, 0);
+  return e == hipSuccess ? nb : 0;
 }
 
 }  // namespace kap

@@ -85,13 +85,31 @@ bool fast_geometry(const kap_kv_cache *kv) {
 struct SplitPlan {
   bool fast;
   int n_split;
-  int pps;  // pages per split
+  int pps;  // most pages any split of the generic path can get
 };
 
 int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
-// Decode: fast path uses 4-wavefront workgroups, ~2 per CU; generic path caps
-// each split at kGenericPagesPerSplit pages.
+// Resident workgroups per CU of a tuned kernel (cached per device).
+// id: 0/1 = decode bf16/fp8; 2 + 4*fp8 + (nt-1) = verify.
+int blocks_per_cu(int id, int kv_type, int q_len) {
+  static std::mutex mu;
+  static int cache[64][10] = {{0}};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  int &c = cache[dev][id];
+  if (c == 0) {
+    const int v = id < 2 ? kap::decode_fast_blocks_per_cu(kv_type)
+                         : kap::verify_mfma_blocks_per_cu(kv_type, q_len);
+    c = v > 0 ? v : -1;
+  }
+  return c > 0 ? c : 0;
+}
+
+// Decode (tuned path): enough (split, KV head, sequence) workgroups to fill
+// every resident slot once; each split keeps >= 4 view pages (one per
+// wavefront). Generic path: splits of at most kGenericPagesPerSplit pages.
 SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num_splits) {
   SplitPlan p{fast_geometry(kv), 1, 1};
   const int mb = max_blocks > 0 ? max_blocks : 1;
@@ -100,13 +118,16 @@ SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num
     if (num_splits > 0) {
       n = num_splits;
     } else {
+      const int fp8 = kv->kv_dtype == KAP_DT_FP8_E4M3FN;
+      int bpc = blocks_per_cu(fp8, fp8 ? kap::kFP8 : kap::kBF16, 1);
+      if (bpc <= 0) bpc = 2;
       const long long work = (long long)batch * kv->num_kv_heads;
-      n = cdiv(2LL * device_cus(), work > 0 ? work : 1);
+      n = (int)((long long)bpc * device_cus() / (work > 0 ? work : 1));
       n = n < cdiv(mb, 4) ? n : cdiv(mb, 4);
     }
     n = n < 1 ? 1 : (n > mb ? mb : n);
+    p.n_split = n;
     p.pps = cdiv(mb, n);
-    p.n_split = cdiv(mb, p.pps);
   } else {
     int n = cdiv(mb, kap::kGenericPagesPerSplit);
     if (num_splits > n) n = num_splits > mb ? mb : num_splits;
@@ -116,8 +137,7 @@ SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num
   return p;
 }
 
-// Verify: fast path uses one wavefront per split, ~8 per CU; pages per split
-// are even (the kernel walks page pairs).
+// Verify (tuned path): as decode, in page pairs, >= 1 pair per wavefront.
 SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_pages, int num_splits) {
   SplitPlan p{fast_geometry(kv) && q_len * 4 <= 64, 1, 1};
   const int mp = max_pages > 0 ? max_pages : 1;
@@ -127,12 +147,17 @@ SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_page
     if (num_splits > 0) {
       n = num_splits;
     } else {
+      const int fp8 = kv->kv_dtype == KAP_DT_FP8_E4M3FN;
+      const int nt = (q_len * 4 + 15) / 16;
+      int bpc = blocks_per_cu(2 + 4 * fp8 + (nt - 1), fp8 ? kap::kFP8 : kap::kBF16, q_len);
+      if (bpc <= 0) bpc = 1;
       const long long work = (long long)batch * kv->num_kv_heads;
-      n = cdiv(8LL * device_cus(), work > 0 ? work : 1);
+      n = (int)((long long)bpc * device_cus() / (work > 0 ? work : 1));
+      n = n < cdiv(pairs, 4) ? n : cdiv(pairs, 4);
     }
     n = n < 1 ? 1 : (n > pairs ? pairs : n);
+    p.n_split = n;
     p.pps = 2 * cdiv(pairs, n);
-    p.n_split = cdiv(mp, p.pps);
   } else {
     int n = cdiv(mp, kap::kGenericPagesPerSplit);
     if (num_splits > n) n = num_splits > mp ? mp : num_splits;
@@ -142,31 +167,48 @@ SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_page
   return p;
 }
 
-size_t partial_bytes(const kap_kv_cache *kv, int batch, int q_len, const SplitPlan &p) {
-  if (p.n_split <= 1 || batch <= 0) return 0;
+// Workspace: [arrival counters, batch*Hkv int32][partial o][partial lse],
+// each part 256-byte aligned. Nothing when there is a single split.
+struct WsLayout {
+  size_t tickets, part_o, part_lse, total;
+};
+
+WsLayout ws_layout(const kap_kv_cache *kv, int batch, int q_len, const SplitPlan &p) {
+  WsLayout w{0, 0, 0, 0};
+  if (p.n_split <= 1 || batch <= 0) return w;
   const size_t rows = (size_t)batch * q_len * kv->num_q_heads;
+  const size_t t = round_up((size_t)batch * kv->num_kv_heads * sizeof(int32_t), 256);
   const size_t o = round_up(rows * p.n_split * kv->head_dim * sizeof(float), 256);
   const size_t l = round_up(rows * p.n_split * sizeof(float), 256);
-  return o + l;
+  w.tickets = 0;
+  w.part_o = t;
+  w.part_lse = t + o;
+  w.total = t + o + l;
+  return w;
 }
 
-kap_status launch_attention(kap::AttnArgs &a, const SplitPlan &p, bool decode, void *ws,
-                            hipStream_t s) {
+size_t partial_bytes(const kap_kv_cache *kv, int batch, int q_len, const SplitPlan &p) {
+  return ws_layout(kv, batch, q_len, p).total;
+}
+
+kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const SplitPlan &p,
+                            bool decode, void *ws, hipStream_t s) {
   a.n_split = p.n_split;
   a.pages_per_split = p.pps;
-  const size_t rows = (size_t)a.batch * a.q_len * a.Hq;
-  a.part_o = static_cast<float *>(ws);
-  a.part_lse = p.n_split > 1
-                   ? reinterpret_cast<float *>(static_cast<char *>(ws) +
-                                               round_up(rows * p.n_split * a.D * sizeof(float), 256))
-                   : nullptr;
+  const WsLayout w = ws_layout(kv, a.batch, a.q_len, p);
+  char *base = static_cast<char *>(ws);
+  a.tickets = w.total ? reinterpret_cast<int32_t *>(base + w.tickets) : nullptr;
+  a.part_o = w.total ? reinterpret_cast<float *>(base + w.part_o) : nullptr;
+  a.part_lse = w.total ? reinterpret_cast<float *>(base + w.part_lse) : nullptr;
   (void)hipGetLastError();  // clear a stale error so a launch failure is ours
   hipError_t e;
-  if (p.fast)
+  if (p.fast) {
+    // the tuned kernels merge their splits themselves
     e = decode ? kap::launch_decode_fast(a, s) : kap::launch_verify_mfma(a, s);
-  else
+  } else {
     e = kap::launch_attn_generic(a, s);
-  if (e == hipSuccess && p.n_split > 1) e = kap::launch_merge(a, s);
+    if (e == hipSuccess && p.n_split > 1) e = kap::launch_merge(a, s);
+  }
   if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }
@@ -290,6 +332,7 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
     return fail(KAP_ERR_INVALID_ARGUMENT, "sm_scale must be finite");
   if (kv->num_q_heads > 65535) return fail(KAP_ERR_UNSUPPORTED, "too many query heads");
   if (batch == 0) return ok();
+  if (kv->num_pages < 1) return fail(KAP_ERR_INVALID_ARGUMENT, "KV pool has no pages");
   if (!q || !seq_lens || !view_num_blocks || !out || !lse)
     return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
   if (max_view_blocks > 0 && (!view_block_table || !view_logical_block))
@@ -327,7 +370,7 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
   a.scale_log2 = sm_scale * kap::kLog2e;
   a.out = out;
   a.lse = lse;
-  return launch_attention(a, p, true, workspace, static_cast<hipStream_t>(stream));
+  return launch_attention(a, kv, p, true, workspace, static_cast<hipStream_t>(stream));
 }
 
 // ---------------------------------------------------------------------------
@@ -361,6 +404,7 @@ kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, cons
     return fail(KAP_ERR_INVALID_ARGUMENT, "sm_scale must be finite");
   if ((long long)q_len * kv->num_q_heads > 65535) return fail(KAP_ERR_UNSUPPORTED, "too many rows");
   if (batch == 0) return ok();
+  if (kv->num_pages < 1) return fail(KAP_ERR_INVALID_ARGUMENT, "KV pool has no pages");
   if (!q || !seq_lens || !out || !lse) return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
   if (max_pages > 0 && !full_block_table)
     return fail(KAP_ERR_INVALID_ARGUMENT, "full_block_table is NULL");
@@ -397,7 +441,7 @@ kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, cons
   a.scale_log2 = sm_scale * kap::kLog2e;
   a.out = out;
   a.lse = lse;
-  return launch_attention(a, p, false, workspace, static_cast<hipStream_t>(stream));
+  return launch_attention(a, kv, p, false, workspace, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

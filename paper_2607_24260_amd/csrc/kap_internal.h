@@ -67,6 +67,7 @@ struct AttnArgs {
   int pages_per_split;
   float *part_o;    // [batch * R][n_split][D]   (normalised partial outputs)
   float *part_lse;  // [batch * R][n_split]      (log2-domain partial LSE)
+  int32_t *tickets; // [batch][Hkv] arrival counters of the fused merge (zero between calls)
   float *out;       // [batch * R][D]
   float *lse;       // [batch * R]
 };
@@ -76,6 +77,11 @@ hipError_t launch_attn_generic(const AttnArgs &a, hipStream_t s);
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s);
 hipError_t launch_verify_mfma(const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(const AttnArgs &a, hipStream_t s);
+
+// Workgroups of the tuned kernels that fit on one compute unit at once
+// (0 if the runtime cannot tell).
+int decode_fast_blocks_per_cu(int kv_type);
+int verify_mfma_blocks_per_cu(int kv_type, int q_len);
 
 // ---------------------------------------------------------------------------
 // device helpers
@@ -117,6 +123,71 @@ __device__ __forceinline__ int wave_sum_i(int x) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
   return x;
+}
+
+// ---------------------------------------------------------------------------
+// fused split merge for the tuned kernels (four query heads per KV head)
+// ---------------------------------------------------------------------------
+
+// Row index (in out / lse) of local row r = 4 * window_token + head_in_group.
+__device__ __forceinline__ size_t out_row(const AttnArgs &a, int b, int g, int r) {
+  return ((size_t)b * a.q_len + (r >> 2)) * a.Hq + g * 4 + (r & 3);
+}
+
+// True in every thread of the workgroup that completes the last of the
+// n_split partials of (b, g). Only wavefront 0 may have written this
+// workgroup's partial: it alone publishes it (agent-scope release, an L2
+// write-back) before taking a ticket, and only the last workgroup acquires
+// (an L2 invalidate) before reading the other partials. The arrival counter is
+// reset to zero by that workgroup.
+__device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, int *flag) {
+  if (threadIdx.x < 64) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (threadIdx.x == 0) {
+      int32_t *ctr = a.tickets + (size_t)b * a.Hkv + g;
+      const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int last = (prev == a.n_split - 1) ? 1 : 0;
+      if (last) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      *flag = last;
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (*reinterpret_cast<volatile int *>(flag)) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  }
+  __syncthreads();
+  return *flag != 0;
+}
+
+// LSE merge of the n_split partials of the R_loc local rows of (b, g), D = 128:
+// lse = log2 sum_s 2^lse_s, o = sum_s 2^(lse_s - lse) o_s (empty splits drop out).
+__device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int R_loc) {
+  for (int e = threadIdx.x; e < R_loc * 32; e += blockDim.x) {
+    const int r = e >> 5, d4 = (e & 31) * 4;
+    const size_t row = out_row(a, b, g, r);
+    const float *pl = a.part_lse + row * a.n_split;
+    float M = -INFINITY;
+    for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, pl[s]);
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    float lse = -INFINITY;
+    if (M != -INFINITY) {
+      float tot = 0.f;
+      const float *po = a.part_o + row * a.n_split * 128 + d4;
+      for (int s = 0; s < a.n_split; ++s) {
+        const float w = exp2f(pl[s] - M);
+        if (w == 0.f) continue;
+        const float4 v = *reinterpret_cast<const float4 *>(po + (size_t)s * 128);
+        tot += w;
+        o.x = fmaf(w, v.x, o.x);
+        o.y = fmaf(w, v.y, o.y);
+        o.z = fmaf(w, v.z, o.z);
+        o.w = fmaf(w, v.w, o.w);
+      }
+      const float inv = 1.f / tot;
+      o.x *= inv; o.y *= inv; o.z *= inv; o.w *= inv;
+      lse = (M + log2f(tot)) * kLn2;
+    }
+    *reinterpret_cast<float4 *>(a.out + row * 128 + d4) = o;
+    if (d4 == 0) a.lse[row] = lse;
+  }
 }
 
 }  // namespace kap

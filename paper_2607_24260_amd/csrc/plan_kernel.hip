@@ -8,8 +8,9 @@
 //      counts, for its spans, how many spans precede them, and writes the
 //      inverse permutation to the workspace,
 //   4. walks the spans in rank order with one wavefront: the 64 lanes test the
-//      span's pages against the bitmap, a wavefront sum gives the cost in
-//      visible tokens, and the span is taken when it fits the budget,
+//      span's pages against the bitmap, a wavefront ballot counts the new
+//      pages (their cost in visible tokens), and the span is taken when it fits
+//      the budget,
 //   5. compacts the bitmap into the ascending logical-page list and maps it
 //      through the full block table.
 // Selection uses integer arithmetic only (float priors are only compared), so
@@ -18,6 +19,8 @@
 
 namespace kap {
 namespace {
+
+constexpr int kRankChunk = 1024;
 
 __device__ __forceinline__ bool ranks_before(float pj, int sj, int j, float pi, int si, int i) {
   if (pj > pi) return true;
@@ -32,6 +35,8 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __shared__ int s_count[kPlanThreads];
   __shared__ long long s_used;
   __shared__ int s_taken;
+  __shared__ float s_prior[kRankChunk];
+  __shared__ int s_start[kRankChunk];
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -87,16 +92,30 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     atomicOr(&bitmap[p >> 5], 1u << (p & 31));
 
   // -- rank the spans ---------------------------------------------------------
+  // rank(i) = number of spans ordered before span i; keys are staged through
+  // LDS in chunks of kRankChunk so the all-pairs count reads LDS broadcasts.
   const int n = hi - lo;
-  for (int i = tid; i < n; i += kPlanThreads) {
-    const float pi = a.span_prior[lo + i];
-    const int si = a.span_start[lo + i];
+  for (int ib = 0; ib < n; ib += kPlanThreads) {
+    const int i = ib + tid;
+    const bool act = i < n;
+    const float pi = act ? a.span_prior[lo + i] : 0.f;
+    const int si = act ? a.span_start[lo + i] : 0;
     int rank = 0;
-    for (int j = 0; j < n; ++j) {
-      rank += ranks_before(a.span_prior[lo + j], a.span_start[lo + j], j, pi, si, i) ? 1 : 0;
+    for (int jb = 0; jb < n; jb += kRankChunk) {
+      __syncthreads();
+      const int jn = min(kRankChunk, n - jb);
+      for (int t = tid; t < jn; t += kPlanThreads) {
+        s_prior[t] = a.span_prior[lo + jb + t];
+        s_start[t] = a.span_start[lo + jb + t];
+      }
+      __syncthreads();
+      if (act)
+        for (int t = 0; t < jn; ++t) rank += ranks_before(s_prior[t], s_start[t], jb + t, pi, si, i);
     }
-    a.perm[lo + rank] = i;
-    if (a.span_selected) a.span_selected[lo + i] = 0;
+    if (act) {
+      a.perm[lo + rank] = i;
+      if (a.span_selected) a.span_selected[lo + i] = 0;
+    }
   }
   __syncthreads();
 
@@ -118,34 +137,52 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __syncthreads();
 
   // -- greedy selection in rank order (one wavefront) -------------------------
+  // Lane l holds the clipped span of rank r0 + l, so one global round trip
+  // serves 64 decisions. Every page except the last (always selected) holds 16
+  // tokens, so a span's cost is 16 x (its pages not yet selected), counted with
+  // a wavefront ballot over 64 pages at a time.
   if (tid < 64) {
     long long used = s_used;
     int taken = 0;
     const long long T = a.budget[b];
-    for (int r = 0; r < n; ++r) {
-      const int i = lo + a.perm[lo + r];
-      const long long st = a.span_start[i];
-      const long long x = st > 0 ? st : 0;
-      long long e = st + (long long)a.span_len[i];
-      if (e > L) e = L;
-      if (e <= x) continue;                               // empty after clipping
-      const int p0 = (int)(x / kPage);
-      const int p1 = (int)((e + kPage - 1) / kPage);
-      int cost = 0;
-      for (int p = p0 + lane; p < p1; p += 64) {
-        const bool sel = (bitmap[p >> 5] >> (p & 31)) & 1u;
-        if (!sel) cost += (p == NP - 1) ? last_valid : kPage;
+    bool stop = false;
+    for (int r0 = 0; r0 < n && !stop; r0 += 64) {
+      int my_i = -1, my_x = 0, my_e = 0;
+      if (r0 + lane < n) {
+        my_i = lo + a.perm[lo + r0 + lane];
+        const long long st = a.span_start[my_i];
+        const long long x = st > 0 ? st : 0;
+        long long e = st + (long long)a.span_len[my_i];
+        if (e > L) e = L;
+        my_x = (int)x;
+        my_e = (int)(e > x ? e : x);                    // e <= x: empty after clipping
       }
-      cost = wave_sum_i(cost);
-      if (used + cost <= T) {
-        for (int p = p0 + lane; p < p1; p += 64) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
-        used += cost;
-        ++taken;
-        if (lane == 0 && a.span_selected) a.span_selected[i] = 1;
-      } else if (a.policy == 1 /*KAP_SELECT_STOP*/) {
-        break;
+      const int cnt = min(64, n - r0);
+      for (int j = 0; j < cnt; ++j) {
+        const int i = __builtin_amdgcn_readlane(my_i, j);
+        const int x = __builtin_amdgcn_readlane(my_x, j);
+        const int e = __builtin_amdgcn_readlane(my_e, j);
+        if (e <= x) continue;                           // ignored
+        const int p0 = x / kPage;
+        const int p1 = (e + kPage - 1) / kPage;
+        int new_pages = 0;
+        for (int p = p0; p < p1; p += 64) {
+          const int pp = p + lane;
+          const bool fresh = pp < p1 && !((bitmap[pp >> 5] >> (pp & 31)) & 1u);
+          new_pages += __popcll(__ballot(fresh));
+        }
+        const long long cost = (long long)kPage * new_pages;
+        if (used + cost <= T) {
+          for (int p = p0 + lane; p < p1; p += 64) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+          used += cost;
+          ++taken;
+          if (lane == 0 && a.span_selected) a.span_selected[i] = 1;
+        } else if (a.policy == 1 /*KAP_SELECT_STOP*/) {
+          stop = true;
+          break;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       }
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
     if (lane == 0) {
       s_used = used;

@@ -4,8 +4,10 @@
 //
 // The q_len window tokens times the four heads of one KV head form
 // R = 4 * q_len query rows that share every key: a real dense contraction.
-// One wavefront owns (key split, KV head, sequence) and walks the split two
-// pages (32 keys) at a time with v_mfma_f32_16x16x32_bf16:
+// A workgroup of four wavefronts owns (key split, KV head, sequence); each
+// wavefront walks its share of the split two pages (32 keys) at a time, with
+// the next page pair's loads in flight (branch-free, so only the older
+// buffer is waited for), using v_mfma_f32_16x16x32_bf16:
 //   S^T[key][row] = K[key][:] . Q[row][:]       A = K tile (16 keys x 32 dims,
 //                                               one 16-byte load per lane),
 //                                               B = Q^T (kept in registers)
@@ -19,6 +21,9 @@
 // steps per page pair. P is split into bf16 hi + lo parts (two PV products),
 // which keeps the probability rounding error below 2^-16 relative.
 // The causal mask and the partial last page are handled on the last pages only.
+// The four wavefronts combine through LDS; with several splits, the workgroup
+// that finishes last for its (sequence, KV head) merges all splits (atomic
+// arrival counter in the workspace), so one launch produces the final output.
 #include "kap_internal.h"
 
 namespace kap {
@@ -94,20 +99,65 @@ __device__ __forceinline__ u32x2 load_vt(const AttnArgs &a, int page, int g, int
   }
 }
 
+// Loaded operands of one page pair (pages k, k+1 of the sequence).
+template <int KV>
+struct PairRegs {
+  u32x4 kA[4], kB[4];
+  u32x2 vA[8], vB[8];
+  int pA, pB;
+  bool okA, okB;
+};
+
+// Pair at pages k, k+1 (k + 1 may lie past the sequence). Invalid page ids
+// read page 0 and are masked by value, so every load is unconditional.
+template <int KV>
+__device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, const int32_t *fbt,
+                                          int k, int k_end, int g, int n, int j) {
+  const int pa = fbt[k];
+  const int pb = (k + 1 < k_end) ? fbt[k + 1] : -1;
+  r.okA = pa >= 0 && (int64_t)pa < a.num_pages;
+  r.okB = pb >= 0 && (int64_t)pb < a.num_pages;
+  r.pA = r.okA ? pa : 0;
+  r.pB = r.okB ? pb : r.pA;
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb) {
+    r.kA[kb] = load_k<KV>(a, r.pA, g, n, j, kb);
+    r.kB[kb] = load_k<KV>(a, r.pB, g, n, j, kb);
+  }
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    r.vA[dt] = load_vt<KV>(a, r.pA, g, dt * 16 + n, j);
+    r.vB[dt] = load_vt<KV>(a, r.pB, g, dt * 16 + n, j);
+  }
+}
+
+constexpr int kVerifyWaves = 4;
+
 template <int KV, int NT>
-__global__ __launch_bounds__(64) void verify_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
+  __shared__ float s_acc[kVerifyWaves][16][kD + 4];
+  __shared__ float s_m[kVerifyWaves][16];
+  __shared__ float s_l[kVerifyWaves][16];
+  __shared__ float s_out[16][kD];
+  __shared__ float s_olse[16];
+  __shared__ int s_flag;
+
   const int split = blockIdx.x;
   const int g = blockIdx.y;
   const int b = blockIdx.z;
-  const int lane = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int n = lane & 15, j = lane >> 4;
   const int R = a.q_len * 4;
 
   const int L = a.seq_lens[b];
   int np_seq = L > 0 ? (int)(((long long)L + kPage - 1) / kPage) : 0;
   np_seq = min(np_seq, a.max_blocks);
-  const int k0 = split * a.pages_per_split;
-  const int k1 = min(np_seq, k0 + a.pages_per_split);
+  // split `split` of n_split takes an even share of this sequence's page pairs;
+  // its four wavefronts take those pairs round-robin
+  const int pairs = (np_seq + 1) / 2;
+  const int q0 = (int)(((long long)split * pairs) / a.n_split);
+  const int q1 = (int)(((long long)(split + 1) * pairs) / a.n_split);
   const int32_t *fbt = a.block_table + (size_t)b * a.bt_stride;
 
   // Q^T operand: row n of each tile, dims 32kb + 8j .. +7
@@ -138,34 +188,26 @@ __global__ __launch_bounds__(64) void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  for (int k = k0; k < k1; k += 2) {
-    const int pA = fbt[k];
-    const int pB = (k + 1 < k1) ? fbt[k + 1] : -1;
-    const bool okA = pA >= 0 && (int64_t)pA < a.num_pages;
-    const bool okB = pB >= 0 && (int64_t)pB < a.num_pages;
+  // Two pair buffers, unrolled by two: while one pair is processed the loads of
+  // the next are in flight. Past the end of this wavefront's pairs the last
+  // pair is re-read (an L2 hit), so the steady state is straight-line code and
+  // only the older buffer's loads are waited for.
+  auto process = [&](PairRegs<KV> &P, int k) {
 
-    // ---- loads: K tiles of both pages and V^T tiles of both pages ------------
-    u32x4 kA[4], kB[4];
-    u32x2 vA[8], vB[8];
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      kA[kb] = okA ? load_k<KV>(a, pA, g, n, j, kb) : u32x4{0u, 0u, 0u, 0u};
-      kB[kb] = okB ? load_k<KV>(a, pB, g, n, j, kb) : u32x4{0u, 0u, 0u, 0u};
-    }
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      vA[dt] = okA ? load_vt<KV>(a, pA, g, dt * 16 + n, j) : u32x2{0u, 0u};
-      vB[dt] = okB ? load_vt<KV>(a, pB, g, dt * 16 + n, j) : u32x2{0u, 0u};
-    }
     float kscA = a.scale_log2, kscB = a.scale_log2, vscA = 1.f, vscB = 1.f;
     if constexpr (KV == kFP8) {
-      if (okA) { kscA *= a.kv_scales[2 * (size_t)pA]; vscA = a.kv_scales[2 * (size_t)pA + 1]; }
-      if (okB) { kscB *= a.kv_scales[2 * (size_t)pB]; vscB = a.kv_scales[2 * (size_t)pB + 1]; }
+      if (P.okA) {
+        kscA *= a.kv_scales[2 * (size_t)P.pA];
+        vscA = a.kv_scales[2 * (size_t)P.pA + 1];
+      }
+      if (P.okB) {
+        kscB *= a.kv_scales[2 * (size_t)P.pB];
+        vscB = a.kv_scales[2 * (size_t)P.pB + 1];
+      }
     }
 
     // keys at or beyond L hold no data: zero their V so 0 * garbage cannot occur
-    const bool tail = (k + 2) * kPage > L;
-    if (tail) {
+    if ((k + 2) * kPage > L) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const bool zA = k * kPage + 4 * j + e >= L;
@@ -173,8 +215,8 @@ __global__ __launch_bounds__(64) void verify_mfma_kernel(AttnArgs a) {
         const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          if (zA) vA[dt][e >> 1] &= mask;
-          if (zB) vB[dt][e >> 1] &= mask;
+          if (zA) P.vA[dt][e >> 1] &= mask;
+          if (zB) P.vB[dt][e >> 1] &= mask;
         }
       }
     }
@@ -187,12 +229,12 @@ __global__ __launch_bounds__(64) void verify_mfma_kernel(AttnArgs a) {
       sB[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        sA[nt] = mfma(kA[kb], qop[nt][kb], sA[nt]);
-        sB[nt] = mfma(kB[kb], qop[nt][kb], sB[nt]);
+        sA[nt] = mfma(P.kA[kb], qop[nt][kb], sA[nt]);
+        sB[nt] = mfma(P.kB[kb], qop[nt][kb], sB[nt]);
       }
     }
 
-    const bool needs_mask = !okA || !okB || (k + 2) > last_full;
+    const bool needs_mask = !P.okA || !P.okB || (k + 2) > last_full;
     u32x4 phi[NT], plo[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -207,8 +249,8 @@ __global__ __launch_bounds__(64) void verify_mfma_kernel(AttnArgs a) {
         for (int e = 0; e < 4; ++e) {
           const int posA = k * kPage + 4 * j + e;
           const int posB = (k + 1) * kPage + 4 * j + e;
-          if (!okA || posA >= lim[nt]) z[e] = -INFINITY;
-          if (!okB || posB >= lim[nt]) z[4 + e] = -INFINITY;
+          if (!P.okA || posA >= lim[nt]) z[e] = -INFINITY;
+          if (!P.okB || posB >= lim[nt]) z[4 + e] = -INFINITY;
         }
       }
       float mx = z[0];
@@ -246,39 +288,98 @@ __global__ __launch_bounds__(64) void verify_mfma_kernel(AttnArgs a) {
     // ---- O^T += V^T P^T -----------------------------------------------------------
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const u32x4 vop = u32x4{vA[dt][0], vA[dt][1], vB[dt][0], vB[dt][1]};
+      const u32x4 vop = u32x4{P.vA[dt][0], P.vA[dt][1], P.vB[dt][0], P.vB[dt][1]};
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         acc[nt][dt] = mfma(vop, phi[nt], acc[nt][dt]);
         acc[nt][dt] = mfma(vop, plo[nt], acc[nt][dt]);
       }
     }
+  };
+
+  const int qw = q0 + wave;
+  const int n_my = qw < q1 ? (q1 - qw + kVerifyWaves - 1) / kVerifyWaves : 0;
+  if (n_my > 0) {
+    auto kpair = [&](int i) { return 2 * (qw + kVerifyWaves * min(i, n_my - 1)); };
+    PairRegs<KV> ra, rb;
+    load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j);
+    load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j);
+    for (int i = 0; i < n_my; i += 2) {
+      process(ra, kpair(i));
+      load_pair<KV>(ra, a, fbt, kpair(i + 2), np_seq, g, n, j);
+      if (i + 1 >= n_my) break;
+      process(rb, kpair(i + 1));
+      load_pair<KV>(rb, a, fbt, kpair(i + 3), np_seq, g, n, j);
+    }
   }
 
-  // ---- write the (partial) result ---------------------------------------------------
+  // ---- combine the four wavefronts, tile by tile, then write ----------------------
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float lt = xor16_sum(l[nt]);
     lt = xor32_sum(lt);
-    const int r = nt * 16 + n;
-    if (r >= R) continue;
-    const int i = r >> 2, hh = r & 3;
-    const size_t row = ((size_t)b * a.q_len + i) * a.Hq + g * 4 + hh;
-    const bool empty = (m[nt] == -INFINITY);
-    const float inv = empty ? 0.f : 1.f / lt;
-    const float lse2 = empty ? -INFINITY : m[nt] + log2f(lt);
-    float *dst = (a.n_split == 1) ? a.out + row * kD
-                                  : a.part_o + (row * a.n_split + split) * kD;
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const f32x4 o = acc[nt][dt] * inv;
-      *reinterpret_cast<f32x4 *>(dst + dt * 16 + 4 * j) = o;
-    }
+    for (int dt = 0; dt < 8; ++dt)
+      *reinterpret_cast<f32x4 *>(&s_acc[wave][n][dt * 16 + 4 * j]) = acc[nt][dt];
     if (j == 0) {
-      if (a.n_split == 1) a.lse[row] = lse2 * kLn2;
-      else a.part_lse[row * a.n_split + split] = lse2;
+      s_m[wave][n] = m[nt];
+      s_l[wave][n] = lt;
     }
+    __syncthreads();
+    const int rn = threadIdx.x >> 4;            // row of the tile
+    const int d8 = (threadIdx.x & 15) * 8;      // 8 dims
+    {
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kVerifyWaves; ++w) M = fmaxf(M, s_m[w][rn]);
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = 0.f;
+      float lse2 = -INFINITY;
+      if (M != -INFINITY) {
+        float den = 0.f;
+#pragma unroll
+        for (int w = 0; w < kVerifyWaves; ++w) {
+          const float ew = exp2f(s_m[w][rn] - M);
+          den = fmaf(ew, s_l[w][rn], den);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[e] = fmaf(ew, s_acc[w][rn][d8 + e], o[e]);
+        }
+        const float inv = 1.f / den;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] *= inv;
+        lse2 = M + log2f(den);
+      }
+      *reinterpret_cast<float4 *>(&s_out[rn][d8]) = make_float4(o[0], o[1], o[2], o[3]);
+      *reinterpret_cast<float4 *>(&s_out[rn][d8 + 4]) = make_float4(o[4], o[5], o[6], o[7]);
+      if (d8 == 0) s_olse[rn] = lse2;
+    }
+    __syncthreads();
+    // wavefront 0 writes the tile (final output, or this split's partial)
+    if (threadIdx.x < 64) {
+#pragma unroll
+      for (int t8 = 0; t8 < 8; ++t8) {
+        const int f = threadIdx.x + 64 * t8;      // float4 index in [16][128]
+        const int rr = f >> 5, d4 = (f & 31) * 4;
+        const int r = nt * 16 + rr;
+        if (r < R) {
+          const size_t row = out_row(a, b, g, r);
+          float *dst = (a.n_split == 1) ? a.out + row * kD + d4
+                                        : a.part_o + (row * a.n_split + split) * kD + d4;
+          *reinterpret_cast<float4 *>(dst) = *reinterpret_cast<const float4 *>(&s_out[rr][d4]);
+        }
+      }
+      if (threadIdx.x < 16 && nt * 16 + threadIdx.x < R) {
+        const size_t row = out_row(a, b, g, nt * 16 + threadIdx.x);
+        if (a.n_split == 1) a.lse[row] = s_olse[threadIdx.x] * kLn2;
+        else a.part_lse[row * a.n_split + split] = s_olse[threadIdx.x];
+      }
+    }
+    __syncthreads();
   }
+
+  // ---- the last workgroup of (b, g) merges the splits ---------------------------------
+  if (a.n_split > 1 && last_arrival(a, b, g, &s_flag)) merge_rows(a, b, g, R);
 }
 
 template <int KV>
@@ -286,13 +387,27 @@ hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
   const dim3 grid(a.n_split, a.Hkv, a.batch);
   const int nt = (a.q_len * 4 + 15) / 16;
   switch (nt) {
-    case 1: hipLaunchKernelGGL((verify_mfma_kernel<KV, 1>), grid, dim3(64), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((verify_mfma_kernel<KV, 2>), grid, dim3(64), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((verify_mfma_kernel<KV, 3>), grid, dim3(64), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((verify_mfma_kernel<KV, 4>), grid, dim3(64), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((verify_mfma_kernel<KV, 1>), grid, dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((verify_mfma_kernel<KV, 2>), grid, dim3(256), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((verify_mfma_kernel<KV, 3>), grid, dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((verify_mfma_kernel<KV, 4>), grid, dim3(256), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <int KV>
+int blocks_kv(int nt) {
+  int nb = 0;
+  hipError_t e = hipErrorInvalidValue;
+  switch (nt) {
+    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 1>, 256, 0); break;
+    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 2>, 256, 0); break;
+    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 3>, 256, 0); break;
+    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 4>, 256, 0); break;
+    default: break;
+  }
+  return e == hipSuccess ? nb : 0;
 }
 
 }  // namespace
@@ -301,6 +416,11 @@ hipError_t launch_verify_mfma(const AttnArgs &a, hipStream_t s) {
   if (a.kv_type == kBF16) return launch_kv<kBF16>(a, s);
   if (a.kv_type == kFP8) return launch_kv<kFP8>(a, s);
   return hipErrorInvalidValue;
+}
+
+int verify_mfma_blocks_per_cu(int kv_type, int q_len) {
+  const int nt = (q_len * 4 + 15) / 16;
+  return kv_type == kFP8 ? blocks_kv<kFP8>(nt) : blocks_kv<kBF16>(nt);
 }
 
 }  // namespace kap

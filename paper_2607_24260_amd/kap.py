@@ -150,8 +150,8 @@ def _stream(stream):
 def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
     if nbytes == 0:
         return workspace, 0
-    if workspace is None:
-        workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    if workspace is None:       # zero-filled: the arrival counters must start at 0
+        workspace = torch.zeros(nbytes, dtype=torch.uint8, device=device)
     _dev(workspace, "workspace")
     have = workspace.numel() * workspace.element_size()
     return workspace, have
@@ -357,3 +357,84 @@ def verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scal
 
 def abi_version() -> int:
     return int(load_library().kap_abi_version())
+
+
+# --------------------------------------------------------------------------
+# pre-marshalled calls (for tight loops and graph capture)
+# --------------------------------------------------------------------------
+
+class BoundCall:
+    """A kap_* call whose ctypes arguments were marshalled once. Calling it
+    re-issues the same launch on the stream captured at bind time; the caller
+    keeps every tensor named at bind time alive."""
+
+    def __init__(self, fn, args, keep):
+        self._fn = fn
+        self._args = args
+        self._keep = keep
+
+    def __call__(self):
+        _check(self._fn(*self._args))
+
+
+def bind_selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
+                         view_num_blocks, max_view_blocks: int, sm_scale: float, out, lse,
+                         workspace=None, num_splits: int = 0, stream=None) -> BoundCall:
+    lib = load_library()
+    selected_decode(kv, q, seq_lens, view_block_table, view_logical_block, view_num_blocks,
+                    max_view_blocks, sm_scale, num_splits=num_splits, out=out, lse=lse,
+                    workspace=workspace, stream=stream)          # validates once
+    need = selected_decode_workspace_bytes(kv, q.shape[0], max_view_blocks, num_splits)
+    have = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if need > have:
+        raise ValueError(f"workspace of {need} bytes required")
+    args = (ctypes.byref(kv.struct), q.shape[0], _ptr(q), _ptr(seq_lens),
+            _ptr(view_block_table), _ptr(view_logical_block), view_block_table.shape[1],
+            _ptr(view_num_blocks), int(max_view_blocks), float(sm_scale), int(num_splits),
+            _ptr(out), _ptr(lse), _ptr(workspace), have, _stream(stream))
+    return BoundCall(lib.kap_selected_decode, args,
+                     (kv, q, seq_lens, view_block_table, view_logical_block, view_num_blocks,
+                      out, lse, workspace))
+
+
+def bind_verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scale: float,
+                out, lse, workspace=None, num_splits: int = 0, stream=None) -> BoundCall:
+    lib = load_library()
+    verify(kv, q, seq_lens, full_block_table, max_seq_len, sm_scale, num_splits=num_splits,
+           out=out, lse=lse, workspace=workspace, stream=stream)
+    need = verify_workspace_bytes(kv, q.shape[0], q.shape[1], max_seq_len, num_splits)
+    have = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if need > have:
+        raise ValueError(f"workspace of {need} bytes required")
+    args = (ctypes.byref(kv.struct), q.shape[0], q.shape[1], _ptr(q), _ptr(seq_lens),
+            _ptr(full_block_table), full_block_table.shape[1], int(max_seq_len),
+            float(sm_scale), int(num_splits), _ptr(out), _ptr(lse), _ptr(workspace), have,
+            _stream(stream))
+    return BoundCall(lib.kap_verify, args,
+                     (kv, q, seq_lens, full_block_table, out, lse, workspace))
+
+
+def bind_compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len,
+                      span_prior, prefix_tokens, suffix_tokens, budget_tokens, *, num_pages: int,
+                      view_capacity: int, out: dict, workspace=None,
+                      policy: int = KAP_SELECT_SKIP, stream=None) -> BoundCall:
+    lib = load_library()
+    compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
+                 prefix_tokens, suffix_tokens, budget_tokens, num_pages=num_pages,
+                 view_capacity=view_capacity, policy=policy, out=out, workspace=workspace,
+                 stream=stream)
+    B, S = seq_lens.shape[0], span_start.shape[0]
+    need = compile_plan_workspace_bytes(B, S, full_block_table.shape[1])
+    have = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if need > have:
+        raise ValueError(f"workspace of {need} bytes required")
+    args = (B, _ptr(seq_lens), _ptr(full_block_table), full_block_table.shape[1],
+            _ptr(span_offsets), S, _ptr(span_start), _ptr(span_len), _ptr(span_prior),
+            _ptr(prefix_tokens), _ptr(suffix_tokens), _ptr(budget_tokens), int(policy),
+            int(num_pages), int(view_capacity), _ptr(out["view_block_table"]),
+            _ptr(out["view_logical_block"]), _ptr(out["view_num_blocks"]),
+            _ptr(out["view_tokens"]), _ptr(out["spans_taken"]), _ptr(out["plan_status"]),
+            _ptr(out.get("span_selected")), _ptr(workspace), have, _stream(stream))
+    return BoundCall(lib.kap_compile_plan, args,
+                     (seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
+                      prefix_tokens, suffix_tokens, budget_tokens, out, workspace))
