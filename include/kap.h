@@ -48,7 +48,9 @@
  *
  * KV cache layout (struct kap_kv_cache)
  * -------------------------------------
- *   k_pages: [num_pages][num_kv_heads][page_size][head_dim]  token-major pages
+ *   k_pages: [num_pages][num_kv_heads][head_dim/8][page_size][8]
+ *            each page's K tile grouped in 8-dim chunks: element
+ *            [p][g][c][t][e] is dim 8c+e of token t
  *   v_pages: [num_pages][num_kv_heads][head_dim][page_size]  dim-major pages
  *   kv_scales (FP8 only): [num_pages][2] float, K scale then V scale; a stored
  *            E4M3FN code x of page p stands for decode(x) * scale.

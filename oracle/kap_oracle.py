@@ -99,7 +99,8 @@ def e4m3fn_to_f64(bits: np.ndarray) -> np.ndarray:
 class KVPool:
     """Stored KV bits, as the GPU library reads them.
 
-    k_pages: [num_pages][Hkv][PAGE][D], token-major within a page.
+    k_pages: [num_pages][Hkv][D/8][PAGE][8]: each page's K tile in 8-dim
+             chunks; element [p][g][c][t][e] is dim 8c+e of token t.
     v_pages: [num_pages][Hkv][D][PAGE], dim-major within a page (each page's
              V tile is stored transposed).
     dtype:   'f32' (float32 arrays), 'bf16' (uint16 bit arrays) or
@@ -124,7 +125,9 @@ class KVPool:
     def keys(self, pages: np.ndarray, g: int) -> np.ndarray:
         """K values of the given physical pages for KV head g: [n][PAGE][D]."""
         pages = np.asarray(pages, dtype=np.int64)
-        k = self._decode(self.k_pages[pages, g])
+        raw = self.k_pages[pages, g]                       # [n][D/8][PAGE][8]
+        n, C, T, E = raw.shape
+        k = self._decode(raw).transpose(0, 2, 1, 3).reshape(n, T, C * E)
         if self.dtype == "fp8":
             k = k * self.scales[pages, 0].astype(np.float64)[:, None, None]
         return k
@@ -285,7 +288,7 @@ def _view_tokens(pool: KVPool, g: int, seq_len: int, pages, lblks):
     pages = np.asarray(pages, dtype=np.int64)
     lblks = np.asarray(lblks, dtype=np.int64)
     if len(pages) == 0:
-        D = pool.k_pages.shape[-1]
+        D = pool.v_pages.shape[2]
         return np.zeros((0, D)), np.zeros((0, D))
     nvalid = np.clip(seq_len - PAGE * lblks, 0, PAGE)
     mask = np.arange(PAGE)[None, :] < nvalid[:, None]         # [n][PAGE]

@@ -69,9 +69,12 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(AttnArgs a) {
     const long long pos = (long long)lb * kPage + tok;
     float z = -INFINITY;
     if (page >= 0 && page < a.num_pages && pos < limit && pos < L) {
-      const size_t kbase = (((size_t)page * a.Hkv + g) * kPage + tok) * D;
+      // K page tile: [D/8 chunks][16 tokens][8 dims]
+      const size_t kbase = ((size_t)page * a.Hkv + g) * kPage * D + (size_t)tok * 8;
       float acc = 0.f;
-      for (int d = 0; d < D; ++d) acc = fmaf(qs[d], load_elem<KV>(a.k_pages, kbase + d), acc);
+      for (int d = 0; d < D; ++d)
+        acc = fmaf(qs[d], load_elem<KV>(a.k_pages, kbase + (size_t)(d >> 3) * (kPage * 8) + (d & 7)),
+                   acc);
       if constexpr (KV == kFP8) acc *= a.kv_scales[2 * (size_t)page];
       z = acc * a.scale_log2;
     }

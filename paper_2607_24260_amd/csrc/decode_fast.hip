@@ -4,7 +4,7 @@
 // Work decomposition: one 256-thread workgroup per (key split, KV head,
 // sequence); split s of n takes view pages [s*nb/n, (s+1)*nb/n) of the
 // sequence's actual view length nb. Its four wavefronts take those pages
-// round-robin (the next page's loads in flight while one is processed), keep
+// round-robin (the next two pages' loads in flight while one is processed), keep
 // their own online-softmax state, and merge through LDS at the end. With more than one
 // split the workgroup writes a partial (o, lse); the workgroup that finishes
 // last for its (sequence, KV head) merges all splits (atomic arrival counter
@@ -12,9 +12,9 @@
 //
 // Per page (16 tokens x 128 dims = 4 KB of bf16 K and 4 KB of V^T):
 //  * K phase: lane (t = lane/4, c = lane%4) loads dims {32i + 8c .. +7}, i<4,
-//    of token t (four 16-byte loads; each instruction reads 64 contiguous
-//    bytes of every token row) and forms partial dot products for the four
-//    query heads with v_dot2_f32_bf16. A transposing reduction inside each
+//    of token t: four 16-byte loads, and since K pages are stored in 8-dim
+//    chunks ([chunk][token][8]) each instruction reads 1 KB contiguously. It
+//    forms partial dot products for the four query heads with v_dot2_f32_bf16. A transposing reduction inside each
 //    lane quad leaves lane (t, c) holding the full logit of token t, head c.
 //  * softmax: page maxima per head come from row rotations plus permlane16 /
 //    permlane32 swaps; the running max, rescale factor and sum are kept per
@@ -88,10 +88,10 @@ __device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, in
                          ((size_t)page * a.Hkv + g) * (kPage * kD);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      r.k[i] = *reinterpret_cast<const u32x4 *>(kb + t * kD + i * 32 + c * 8);
+      r.k[i] = load_stream(reinterpret_cast<const u32x4 *>(kb + (4 * i + c) * 128 + t * 8));
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      r.v[i] = *reinterpret_cast<const u32x4 *>(vb + i * 512 + lane * 8);
+      r.v[i] = load_stream(reinterpret_cast<const u32x4 *>(vb + i * 512 + lane * 8));
   } else {
     const uint8_t *kb = static_cast<const uint8_t *>(a.k_pages) +
                         ((size_t)page * a.Hkv + g) * (kPage * kD);
@@ -99,10 +99,10 @@ __device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, in
                         ((size_t)page * a.Hkv + g) * (kPage * kD);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      r.k[i] = *reinterpret_cast<const u32x2 *>(kb + t * kD + i * 32 + c * 8);
+      r.k[i] = load_stream(reinterpret_cast<const u32x2 *>(kb + (4 * i + c) * 128 + t * 8));
 #pragma unroll
     for (int i = 0; i < 4; ++i)
-      r.v[i] = *reinterpret_cast<const u32x2 *>(vb + i * 512 + lane * 8);
+      r.v[i] = load_stream(reinterpret_cast<const u32x2 *>(vb + i * 512 + lane * 8));
   }
 }
 
@@ -293,28 +293,35 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
 
-  // Two page buffers, unrolled by two: while one page is processed the loads of
-  // the next are in flight. Loads are unconditional (past the end of this
-  // wavefront's pages the last page is re-read, an L2 hit) so the steady state
-  // is straight-line code and only the older buffer's loads are waited for.
+  // Three page buffers, unrolled by three: while one page is processed the
+  // loads of the next two are in flight. Loads are unconditional (past the end
+  // of this wavefront's pages the last page is re-read, an L2 hit) so the
+  // steady state is straight-line code and only the oldest buffer's loads are
+  // waited for.
   const int kw = k0 + wave;
   const int n_my = kw < k1 ? (k1 - kw + kWaves - 1) / kWaves : 0;
   if (n_my > 0) {
     auto kidx = [&](int i) { return kw + kWaves * min(i, n_my - 1); };
-    PageRegs<KV> ra, rb;
-    int pga, nva, pgb, nvb;
+    PageRegs<KV> ra, rb, rc;
+    int pga, nva, pgb, nvb, pgc, nvc;
     page_info(kidx(0), pga, nva);
     load_page<KV>(ra, a, pga, g, lane);
     page_info(kidx(1), pgb, nvb);
     load_page<KV>(rb, a, pgb, g, lane);
-    for (int i = 0; i < n_my; i += 2) {
+    page_info(kidx(2), pgc, nvc);
+    load_page<KV>(rc, a, pgc, g, lane);
+    for (int i = 0; i < n_my; i += 3) {
       process(ra, pga, nva);
-      page_info(kidx(i + 2), pga, nva);
+      page_info(kidx(i + 3), pga, nva);
       load_page<KV>(ra, a, pga, g, lane);
       if (i + 1 >= n_my) break;
       process(rb, pgb, nvb);
-      page_info(kidx(i + 3), pgb, nvb);
+      page_info(kidx(i + 4), pgb, nvb);
       load_page<KV>(rb, a, pgb, g, lane);
+      if (i + 2 >= n_my) break;
+      process(rc, pgc, nvc);
+      page_info(kidx(i + 5), pgc, nvc);
+      load_page<KV>(rc, a, pgc, g, lane);
     }
   }
 

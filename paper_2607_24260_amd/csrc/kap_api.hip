@@ -107,9 +107,9 @@ int blocks_per_cu(int id, int kv_type, int q_len) {
   return c > 0 ? c : 0;
 }
 
-// Decode (tuned path): enough (split, KV head, sequence) workgroups to fill
-// every resident slot once; each split keeps >= 4 view pages (one per
-// wavefront). Generic path: splits of at most kGenericPagesPerSplit pages.
+// Decode (tuned path): about one (split, KV head, sequence) workgroup per
+// CU; each split keeps >= 4 view pages (one per wavefront). Generic path:
+// splits of at most kGenericPagesPerSplit pages.
 SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num_splits) {
   SplitPlan p{fast_geometry(kv), 1, 1};
   const int mb = max_blocks > 0 ? max_blocks : 1;
@@ -118,11 +118,10 @@ SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num
     if (num_splits > 0) {
       n = num_splits;
     } else {
-      const int fp8 = kv->kv_dtype == KAP_DT_FP8_E4M3FN;
-      int bpc = blocks_per_cu(fp8, fp8 ? kap::kFP8 : kap::kBF16, 1);
-      if (bpc <= 0) bpc = 2;
+      // one workgroup per CU: short splits pay more in fixed per-workgroup
+      // work (query load, combine, merge ticket) than extra occupancy returns
       const long long work = (long long)batch * kv->num_kv_heads;
-      n = (int)((long long)bpc * device_cus() / (work > 0 ? work : 1));
+      n = (int)((long long)device_cus() / (work > 0 ? work : 1));
       n = n < cdiv(mb, 4) ? n : cdiv(mb, 4);
     }
     n = n < 1 ? 1 : (n > mb ? mb : n);

@@ -29,10 +29,33 @@ __device__ __forceinline__ bool ranks_before(float pj, int sj, int j, float pi, 
   return j < i;
 }
 
+// Exclusive prefix sum of v over the workgroup (kPlanThreads threads, in
+// thread order); *total receives the sum. s_tmp holds kPlanThreads/64 ints.
+__device__ __forceinline__ int block_exclusive_scan(int v, int *s_tmp, int *total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_tmp[w] = x;
+  __syncthreads();
+  int before = 0, all = 0;
+#pragma unroll
+  for (int i = 0; i < kPlanThreads / 64; ++i) {
+    before += (i < w) ? s_tmp[i] : 0;
+    all += s_tmp[i];
+  }
+  __syncthreads();
+  *total = all;
+  return before + x - v;
+}
+
 __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) {
   extern __shared__ uint32_t bitmap[];
   __shared__ int s_flag;
-  __shared__ int s_count[kPlanThreads];
+  __shared__ int s_scan[kPlanThreads / 64];
   __shared__ long long s_used;
   __shared__ int s_taken;
   __shared__ float s_prior[kRankChunk];
@@ -124,15 +147,13 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   {
     int c = 0;
     for (int w = tid; w < W; w += kPlanThreads) c += __popc(bitmap[w]);
-    s_count[tid] = c;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int c = 0;
-    for (int t = 0; t < kPlanThreads; ++t) c += s_count[t];
-    // the last page is always selected (suffix >= 1 token)
-    s_used = (long long)kPage * c - (kPage - last_valid);
-    s_taken = 0;
+    int total = 0;
+    block_exclusive_scan(c, s_scan, &total);
+    if (tid == 0) {
+      // the last page is always selected (suffix >= 1 token)
+      s_used = (long long)kPage * total - (kPage - last_valid);
+      s_taken = 0;
+    }
   }
   __syncthreads();
 
@@ -197,26 +218,14 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   const int w1 = min(W, w0 + chunk);
   int mine = 0;
   for (int w = w0; w < w1; ++w) mine += __popc(bitmap[w]);
-  s_count[tid] = mine;
   if (tid == 0) s_flag = 0;
-  __syncthreads();
-  if (tid == 0) {                                         // exclusive scan (256 entries)
-    int run = 0;
-    for (int t = 0; t < kPlanThreads; ++t) {
-      const int c = s_count[t];
-      s_count[t] = run;
-      run += c;
-    }
-    s_flag = 0;
-    bitmap[W] = (uint32_t)run;                            // spare word: total count
-  }
-  __syncthreads();
-  const int nblk = (int)bitmap[W];
+  int nblk = 0;
+  const int first = block_exclusive_scan(mine, s_scan, &nblk);
   if (nblk > a.capacity) {
     write_fail(1 /*KAP_PLAN_OVER_CAPACITY*/, true);
     return;
   }
-  int out = s_count[tid];
+  int out = first;
   const int32_t *fbt_row = a.fbt + (size_t)b * a.fbt_stride;
   int32_t *vbt = a.view_bt + (size_t)b * a.capacity;
   int32_t *vlb = a.view_lblk + (size_t)b * a.capacity;

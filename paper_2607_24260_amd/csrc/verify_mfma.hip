@@ -6,10 +6,12 @@
 // R = 4 * q_len query rows that share every key: a real dense contraction.
 // A workgroup of four wavefronts owns (key split, KV head, sequence); each
 // wavefront walks its share of the split two pages (32 keys) at a time, with
-// the next page pair's loads in flight (branch-free, so only the older
+// the next two page pairs' loads in flight (branch-free, so only the oldest
 // buffer is waited for), using v_mfma_f32_16x16x32_bf16:
 //   S^T[key][row] = K[key][:] . Q[row][:]       A = K tile (16 keys x 32 dims,
-//                                               one 16-byte load per lane),
+//                                               one 16-byte load per lane; K
+//                                               pages in 8-dim chunks make it
+//                                               1 KB contiguous per load),
 //                                               B = Q^T (kept in registers)
 //   O^T[dim][row] += V^T[dim][key] P^T[key][row] A = V^T tile (dim-major pages:
 //                                               4 keys = 8 contiguous bytes),
@@ -74,12 +76,12 @@ template <int KV>
 __device__ __forceinline__ u32x4 load_k(const AttnArgs &a, int page, int g, int n, int j, int kb) {
   if constexpr (KV == kBF16) {
     const uint16_t *p = static_cast<const uint16_t *>(a.k_pages) +
-                        ((size_t)page * a.Hkv + g) * (kPage * kD) + n * kD + kb * 32 + j * 8;
-    return *reinterpret_cast<const u32x4 *>(p);
+                        ((size_t)page * a.Hkv + g) * (kPage * kD) + (kb * 4 + j) * 128 + n * 8;
+    return load_stream(reinterpret_cast<const u32x4 *>(p));
   } else {
     const uint8_t *p = static_cast<const uint8_t *>(a.k_pages) +
-                       ((size_t)page * a.Hkv + g) * (kPage * kD) + n * kD + kb * 32 + j * 8;
-    const u32x2 w = *reinterpret_cast<const u32x2 *>(p);
+                       ((size_t)page * a.Hkv + g) * (kPage * kD) + (kb * 4 + j) * 128 + n * 8;
+    const u32x2 w = load_stream(reinterpret_cast<const u32x2 *>(p));
     const u32x2 lo = fp8x4_to_bf16x4(w[0]), hi = fp8x4_to_bf16x4(w[1]);
     return u32x4{lo[0], lo[1], hi[0], hi[1]};
   }
@@ -91,11 +93,11 @@ __device__ __forceinline__ u32x2 load_vt(const AttnArgs &a, int page, int g, int
   if constexpr (KV == kBF16) {
     const uint16_t *p = static_cast<const uint16_t *>(a.v_pages) +
                         ((size_t)page * a.Hkv + g) * (kPage * kD) + d * kPage + j * 4;
-    return *reinterpret_cast<const u32x2 *>(p);
+    return load_stream(reinterpret_cast<const u32x2 *>(p));
   } else {
     const uint8_t *p = static_cast<const uint8_t *>(a.v_pages) +
                        ((size_t)page * a.Hkv + g) * (kPage * kD) + d * kPage + j * 4;
-    return fp8x4_to_bf16x4(*reinterpret_cast<const uint32_t *>(p));
+    return fp8x4_to_bf16x4(load_stream(reinterpret_cast<const uint32_t *>(p)));
   }
 }
 
@@ -188,10 +190,10 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  // Two pair buffers, unrolled by two: while one pair is processed the loads of
-  // the next are in flight. Past the end of this wavefront's pairs the last
-  // pair is re-read (an L2 hit), so the steady state is straight-line code and
-  // only the older buffer's loads are waited for.
+  // Three pair buffers (two for 9..12-token windows, one beyond), unrolled:
+  // while one pair is processed the loads of the next ones are in flight. Past the end of this wavefront's
+  // pairs the last pair is re-read (an L2 hit), so the steady state is
+  // straight-line code and only the oldest buffer's loads are waited for.
   auto process = [&](PairRegs<KV> &P, int k) {
 
     float kscA = a.scale_log2, kscB = a.scale_log2, vscA = 1.f, vscB = 1.f;
@@ -301,15 +303,38 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   const int n_my = qw < q1 ? (q1 - qw + kVerifyWaves - 1) / kVerifyWaves : 0;
   if (n_my > 0) {
     auto kpair = [&](int i) { return 2 * (qw + kVerifyWaves * min(i, n_my - 1)); };
-    PairRegs<KV> ra, rb;
-    load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j);
-    load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j);
-    for (int i = 0; i < n_my; i += 2) {
-      process(ra, kpair(i));
-      load_pair<KV>(ra, a, fbt, kpair(i + 2), np_seq, g, n, j);
-      if (i + 1 >= n_my) break;
-      process(rb, kpair(i + 1));
-      load_pair<KV>(rb, a, fbt, kpair(i + 3), np_seq, g, n, j);
+    if constexpr (NT <= 2) {
+      PairRegs<KV> ra, rb, rc;
+      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j);
+      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j);
+      load_pair<KV>(rc, a, fbt, kpair(2), np_seq, g, n, j);
+      for (int i = 0; i < n_my; i += 3) {
+        process(ra, kpair(i));
+        load_pair<KV>(ra, a, fbt, kpair(i + 3), np_seq, g, n, j);
+        if (i + 1 >= n_my) break;
+        process(rb, kpair(i + 1));
+        load_pair<KV>(rb, a, fbt, kpair(i + 4), np_seq, g, n, j);
+        if (i + 2 >= n_my) break;
+        process(rc, kpair(i + 2));
+        load_pair<KV>(rc, a, fbt, kpair(i + 5), np_seq, g, n, j);
+      }
+    } else if constexpr (NT == 4) {   // 13..16-token windows: one buffer
+      PairRegs<KV> ra;
+      for (int i = 0; i < n_my; ++i) {
+        load_pair<KV>(ra, a, fbt, kpair(i), np_seq, g, n, j);
+        process(ra, kpair(i));
+      }
+    } else {   // 9..12-token windows hold more accumulators: two buffers
+      PairRegs<KV> ra, rb;
+      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j);
+      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j);
+      for (int i = 0; i < n_my; i += 2) {
+        process(ra, kpair(i));
+        load_pair<KV>(ra, a, fbt, kpair(i + 2), np_seq, g, n, j);
+        if (i + 1 >= n_my) break;
+        process(rb, kpair(i + 1));
+        load_pair<KV>(rb, a, fbt, kpair(i + 3), np_seq, g, n, j);
+      }
     }
   }
 

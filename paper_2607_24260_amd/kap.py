@@ -168,8 +168,9 @@ _Q_DT = {torch.float32: KAP_DT_F32, torch.bfloat16: KAP_DT_BF16}
 
 @dataclass
 class KVCache:
-    """Paged KV pool: k_pages [P][Hkv][16][D], v_pages [P][Hkv][D][16];
-    fp8 pools are uint8 (E4M3FN codes) with kv_scales [P][2] float32."""
+    """Paged KV pool: k_pages [P][Hkv][D/8][16][8] (8-dim chunks, then
+    tokens), v_pages [P][Hkv][D][16]; fp8 pools are uint8 (E4M3FN codes) with
+    kv_scales [P][2] float32."""
     k_pages: torch.Tensor
     v_pages: torch.Tensor
     num_q_heads: int
@@ -177,9 +178,12 @@ class KVCache:
     kv_scales: Optional[torch.Tensor] = None
 
     def __post_init__(self):
-        _dev(self.k_pages, "k_pages", ndim=4)
+        _dev(self.k_pages, "k_pages", ndim=5)
         _dev(self.v_pages, "v_pages", ndim=4)
-        P, Hkv, page, D = self.k_pages.shape
+        P, Hkv, C, page, E = self.k_pages.shape
+        D = C * E
+        if E != 8:
+            raise ValueError("k_pages must be [P][Hkv][D/8][page][8]")
         if tuple(self.v_pages.shape) != (P, Hkv, D, page):
             raise ValueError(f"v_pages must be [P][Hkv][D][page] = {(P, Hkv, D, page)}, "
                              f"got {tuple(self.v_pages.shape)}")

@@ -23,8 +23,8 @@ available, so everything here is synthetic:
   OCP E4M3FN by torch; the per-page scales are stored in float32.
 
 KV layout (as stored for the library):
-  k_pages [num_pages][Hkv][16][D]   token-major within a page
-  v_pages [num_pages][Hkv][D][16]   dim-major within a page
+  k_pages [num_pages][Hkv][D/8][16][8]  8-dim chunks, then tokens, within a page
+  v_pages [num_pages][Hkv][D][16]       dim-major within a page
 """
 from __future__ import annotations
 
@@ -125,7 +125,7 @@ def kv_pool(num_pages: int, Hkv: int, D: int, dtype: str, seed: int, device):
     gen = torch.Generator(device=device)
     gen.manual_seed(seed)
     store = KV_STORAGE[dtype]
-    k = torch.empty((num_pages, Hkv, PAGE, D), dtype=store, device=device)
+    k = torch.empty((num_pages, Hkv, D // 8, PAGE, 8), dtype=store, device=device)
     v = torch.empty((num_pages, Hkv, D, PAGE), dtype=store, device=device)
     scales = (torch.empty((num_pages, 2), dtype=torch.float32, device=device)
               if dtype == "fp8" else None)
@@ -140,9 +140,9 @@ def kv_pool(num_pages: int, Hkv: int, D: int, dtype: str, seed: int, device):
             elif dtype == "bf16":
                 dst[p0:p1] = x.to(torch.bfloat16)
             else:
-                amax = x.abs().amax(dim=(1, 2, 3))
+                amax = x.abs().flatten(1).amax(dim=1)
                 sc = amax / 448.0
-                y = (x / sc[:, None, None, None]).clamp_(-448.0, 448.0)
+                y = (x / sc.view(-1, *([1] * (x.dim() - 1)))).clamp_(-448.0, 448.0)
                 dst[p0:p1] = y.to(torch.float8_e4m3fn).view(torch.uint8)
                 scales[p0:p1, which] = sc
     return k, v, scales

@@ -278,11 +278,12 @@ def test_peaky_planted_keys(alpha, kv_dtype):
             for g in range(w.num_kv_heads):
                 h = g * 4 + int(rng.integers(0, 4))
                 vec = alpha * q[b, h] / (q[b, h] @ q[b, h])
+                vec = vec.view(-1, 8)                       # K pages hold 8-dim chunks
                 if kv_dtype == "bf16":
-                    k[page, g, slot] = vec.to(torch.bfloat16)
+                    k[page, g, :, slot] = vec.to(torch.bfloat16)
                 else:
                     sc = float(w.kv_scales[0][page, 0])
-                    k[page, g, slot] = (vec / sc).clamp(-448, 448).to(
+                    k[page, g, :, slot] = (vec / sc).clamp(-448, 448).to(
                         torch.float8_e4m3fn).view(torch.uint8)
     pool = oracle_pool(w)
     _CACHE.clear()

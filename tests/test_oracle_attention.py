@@ -30,8 +30,9 @@ P = 16
 # --------------------------------------------------------------------------
 
 def make_pool(num_pages, Hkv, D, dtype, seed):
+    """Random pool in the stored layout: K [P][Hkv][D/8][16][8], V [P][Hkv][D][16]."""
     g = torch.Generator().manual_seed(seed)
-    k = torch.randn((num_pages, Hkv, P, D), generator=g)
+    k = torch.randn((num_pages, Hkv, D // 8, P, 8), generator=g)
     v = torch.randn((num_pages, Hkv, D, P), generator=g)
     if dtype == "f32":
         return O.KVPool(k.numpy(), v.numpy(), "f32")
@@ -39,16 +40,23 @@ def make_pool(num_pages, Hkv, D, dtype, seed):
         kb = k.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
         vb = v.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
         return O.KVPool(kb, vb, "bf16")
-    sk = (k.abs().amax(dim=(1, 2, 3)) / 448.0)
-    sv = (v.abs().amax(dim=(1, 2, 3)) / 448.0)
-    kq = (k / sk[:, None, None, None]).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    sk = k.abs().flatten(1).amax(dim=1) / 448.0
+    sv = v.abs().flatten(1).amax(dim=1) / 448.0
+    kq = (k / sk[:, None, None, None, None]).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     vq = (v / sv[:, None, None, None]).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
     return O.KVPool(kq, vq, "fp8", torch.stack([sk, sv], 1).numpy())
 
 
+def key_vec(pool, page, g, t):
+    """Stored K of token t (float64), read from the chunked layout by hand."""
+    return np.concatenate([pool.k_pages[page, g, c, t] for c in range(pool.k_pages.shape[2])]
+                          ).astype(np.float64)
+
+
 def torch_values(pool):
     """Pool contents as fp64 torch tensors via torch's own dtype decoders:
-    K [pages][Hkv][P][D], V [pages][Hkv][P][D] (V transposed back)."""
+    K [pages][Hkv][P][D] (chunks merged back), V [pages][Hkv][P][D]
+    (V transposed back)."""
     if pool.dtype == "f32":
         k, v = torch.from_numpy(pool.k_pages), torch.from_numpy(pool.v_pages)
     elif pool.dtype == "bf16":
@@ -57,7 +65,9 @@ def torch_values(pool):
     else:
         k = torch.from_numpy(pool.k_pages).view(torch.float8_e4m3fn)
         v = torch.from_numpy(pool.v_pages).view(torch.float8_e4m3fn)
-    k, v = k.to(torch.float64), v.to(torch.float64).transpose(2, 3)
+    nP, H, C, T, E = k.shape
+    k = k.to(torch.float64).permute(0, 1, 3, 2, 4).reshape(nP, H, T, C * E)
+    v = v.to(torch.float64).transpose(2, 3)
     if pool.dtype == "fp8":
         sc = torch.from_numpy(pool.scales).to(torch.float64)
         k = k * sc[:, 0, None, None, None]
@@ -208,7 +218,7 @@ def test_single_visible_token():
     fbt = np.array([[2, 0]])
     q = np.random.default_rng(0).standard_normal((1, 1, 8))
     o, lse = O.selected_decode(pool, q, [17], [[0]], [[1]], [1], 0.5)
-    k16 = pool.k_pages[0, 0, 0].astype(np.float64)
+    k16 = key_vec(pool, 0, 0, 0)
     v16 = pool.v_pages[0, 0, :, 0].astype(np.float64)
     np.testing.assert_allclose(o[0, 0], v16, atol=1e-15)
     assert abs(lse[0, 0] - 0.5 * float(q[0, 0] @ k16)) < 1e-14
@@ -228,10 +238,10 @@ def test_constant_keys_give_mean():
 
 
 def test_two_tokens_sigmoid():
-    pool = make_pool(1, 1, 4, "f32", 5)
-    q = np.array([[[[0.3, -1.2, 0.7, 2.0]]]])
+    pool = make_pool(1, 1, 8, "f32", 5)
+    q = np.array([[[[0.3, -1.2, 0.7, 2.0, -0.4, 0.1, 0.9, -1.5]]]])
     o, lse = O.verify(pool, q, [2], [[0]], 1.3)
-    k1, k2 = pool.k_pages[0, 0, 0].astype(float), pool.k_pages[0, 0, 1].astype(float)
+    k1, k2 = key_vec(pool, 0, 0, 0), key_vec(pool, 0, 0, 1)
     v1, v2 = pool.v_pages[0, 0, :, 0].astype(float), pool.v_pages[0, 0, :, 1].astype(float)
     z1, z2 = 1.3 * q[0, 0, 0] @ k1, 1.3 * q[0, 0, 0] @ k2
     sig = 1.0 / (1.0 + math.exp(-(z1 - z2)))
@@ -240,8 +250,8 @@ def test_two_tokens_sigmoid():
 
 
 def test_empty_view_row():
-    pool = make_pool(2, 1, 4, "f32", 6)
-    o, lse = O.selected_decode(pool, np.ones((1, 1, 4)), [20], [[0]], [[0]], [0], 1.0)
+    pool = make_pool(2, 1, 8, "f32", 6)
+    o, lse = O.selected_decode(pool, np.ones((1, 1, 8)), [20], [[0]], [[0]], [0], 1.0)
     assert np.all(o == 0) and lse[0, 0] == -np.inf
 
 
