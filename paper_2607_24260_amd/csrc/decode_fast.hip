@@ -81,28 +81,21 @@ template <int KV>
 __device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, int page, int g,
                                           int lane) {
   const int t = lane >> 2, c = lane & 3;
+  constexpr int kTile = (KV == kBF16 ? 2 : 1) * kPage * kD;   // bytes per (page, head) tile
+  const size_t off = ((size_t)page * a.Hkv + g) * kTile;
+  const auto kr = tile_rsrc(a.k_pages, off, kTile);
+  const auto vr = tile_rsrc(a.v_pages, off, kTile);
   if constexpr (KV == kBF16) {
-    const uint16_t *kb = static_cast<const uint16_t *>(a.k_pages) +
-                         ((size_t)page * a.Hkv + g) * (kPage * kD);
-    const uint16_t *vb = static_cast<const uint16_t *>(a.v_pages) +
-                         ((size_t)page * a.Hkv + g) * (kPage * kD);
+    // K: chunk 4i + c of token t; V^T: 1 KB row block i, 16 bytes per lane
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      r.k[i] = load_stream(reinterpret_cast<const u32x4 *>(kb + (4 * i + c) * 128 + t * 8));
+    for (int i = 0; i < 4; ++i) r.k[i] = tile_load16(kr, i * 1024 + c * 256 + t * 16);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      r.v[i] = load_stream(reinterpret_cast<const u32x4 *>(vb + i * 512 + lane * 8));
+    for (int i = 0; i < 4; ++i) r.v[i] = tile_load16(vr, i * 1024 + lane * 16);
   } else {
-    const uint8_t *kb = static_cast<const uint8_t *>(a.k_pages) +
-                        ((size_t)page * a.Hkv + g) * (kPage * kD);
-    const uint8_t *vb = static_cast<const uint8_t *>(a.v_pages) +
-                        ((size_t)page * a.Hkv + g) * (kPage * kD);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      r.k[i] = load_stream(reinterpret_cast<const u32x2 *>(kb + (4 * i + c) * 128 + t * 8));
+    for (int i = 0; i < 4; ++i) r.k[i] = tile_load8(kr, i * 512 + c * 128 + t * 8);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      r.v[i] = load_stream(reinterpret_cast<const u32x2 *>(vb + i * 512 + lane * 8));
+    for (int i = 0; i < 4; ++i) r.v[i] = tile_load8(vr, i * 512 + lane * 8);
   }
 }
 
@@ -378,17 +371,18 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   if ((threadIdx.x & 63) == 0) s_plse[hh] = lse2;
   __syncthreads();
   if (threadIdx.x < 64) {
+    const auto ro = partial_rsrc(a.part_o);
+    const auto rl = partial_rsrc(a.part_lse);
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
       const int f = threadIdx.x + 64 * t2;       // float4 index in [4][128]
       const int h4 = f >> 5, d4 = (f & 31) * 4;
       const size_t pr = ((size_t)b * a.Hq + g * 4 + h4) * a.n_split + split;
-      *reinterpret_cast<float4 *>(a.part_o + pr * kD + d4) =
-          *reinterpret_cast<const float4 *>(&s_part[h4][d4]);
+      partial_store4(ro, (pr * kD + d4) * 4, *reinterpret_cast<const float4 *>(&s_part[h4][d4]));
     }
     if (threadIdx.x < 4) {
       const size_t pr = ((size_t)b * a.Hq + g * 4 + threadIdx.x) * a.n_split + split;
-      a.part_lse[pr] = s_plse[threadIdx.x];
+      partial_store1(rl, pr * 4, s_plse[threadIdx.x]);
     }
   }
   if (last_arrival(a, b, g, &s_flag)) merge_rows(a, b, g, 4);

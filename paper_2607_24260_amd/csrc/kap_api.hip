@@ -195,6 +195,9 @@ kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const Spli
   a.n_split = p.n_split;
   a.pages_per_split = p.pps;
   const WsLayout w = ws_layout(kv, a.batch, a.q_len, p);
+  if (p.fast && w.total > 0x7fffffffULL)
+    return fail(KAP_ERR_UNSUPPORTED, "split partials need %zu bytes (> 2 GiB); pass fewer splits",
+                w.total);
   char *base = static_cast<char *>(ws);
   a.tickets = w.total ? reinterpret_cast<int32_t *>(base + w.tickets) : nullptr;
   a.part_o = w.total ? reinterpret_cast<float *>(base + w.part_o) : nullptr;

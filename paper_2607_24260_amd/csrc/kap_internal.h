@@ -94,6 +94,30 @@ __device__ __forceinline__ T load_stream(const T *p) {
   return __builtin_nontemporal_load(p);
 }
 
+// Buffer descriptor of one (page, KV head) tile of `bytes` bytes at
+// base + byte_off (wave-uniform). Loads through it take a per-lane byte
+// offset, are bounds-checked by the hardware (reads past `bytes` return 0) and
+// need no per-page vector address arithmetic.
+typedef uint32_t kv_u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t kv_u32x2 __attribute__((ext_vector_type(2)));
+constexpr int kBufDword3 = 0x00020000;   // raw 32-bit buffer, gfx9 family
+constexpr int kNonTemporal = 2;          // cache-policy bit: no temporal reuse
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void *base, size_t byte_off,
+                                                            int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char *>(static_cast<const char *>(base) + byte_off), 0, bytes, kBufDword3);
+}
+__device__ __forceinline__ kv_u32x4 tile_load16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(kv_u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal));
+}
+__device__ __forceinline__ kv_u32x2 tile_load8(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(kv_u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kNonTemporal));
+}
+__device__ __forceinline__ uint32_t tile_load4(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kNonTemporal);
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -141,15 +165,43 @@ __device__ __forceinline__ size_t out_row(const AttnArgs &a, int b, int g, int r
   return ((size_t)b * a.q_len + (r >> 2)) * a.Hq + g * 4 + (r & 3);
 }
 
+// Partial results travel between workgroups with stores and loads that carry
+// the agent-scope coherence bit (sc1): the bit the AMDGPU memory model uses
+// for agent-scope atomic stores and loads. Such stores are written through to
+// the device-coherent level and such loads bypass non-coherent cached copies,
+// so no L2 write-back or invalidate (whose cost grows with the number of
+// workgroups) is needed; a vmcnt(0) wait orders the partial stores before the
+// arrival ticket.
+constexpr int kCoherent = 16;   // sc1
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t partial_rsrc(const float *base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), 0, 0x7fffffff, kBufDword3);
+}
+__device__ __forceinline__ void partial_store4(__amdgpu_buffer_rsrc_t r, size_t byte_off,
+                                               float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(kv_u32x4, v), r, (int)byte_off, 0,
+                                         kCoherent);
+}
+__device__ __forceinline__ void partial_store1(__amdgpu_buffer_rsrc_t r, size_t byte_off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, (int)byte_off, 0, kCoherent);
+}
+__device__ __forceinline__ float4 partial_load4(__amdgpu_buffer_rsrc_t r, size_t byte_off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0,
+                                                                          kCoherent));
+}
+__device__ __forceinline__ float partial_load1(__amdgpu_buffer_rsrc_t r, size_t byte_off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, kCoherent));
+}
+
 // True in every thread of the workgroup that completes the last of the
 // n_split partials of (b, g). Only wavefront 0 may have written this
-// workgroup's partial: it alone publishes it (agent-scope release, an L2
-// write-back) before taking a ticket, and only the last workgroup acquires
-// (an L2 invalidate) before reading the other partials. The arrival counter is
-// reset to zero by that workgroup.
+// workgroup's partial (with partial_store*): it waits until those stores are
+// complete, then takes a ticket. The last workgroup resets the counter.
 __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, int *flag) {
   if (threadIdx.x < 64) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores are complete
+    asm volatile("" ::: "memory");
     if (threadIdx.x == 0) {
       int32_t *ctr = a.tickets + (size_t)b * a.Hkv + g;
       const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -157,8 +209,6 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
       if (last) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       *flag = last;
     }
-    __builtin_amdgcn_wave_barrier();
-    if (*reinterpret_cast<volatile int *>(flag)) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   }
   __syncthreads();
   return *flag != 0;
@@ -167,21 +217,23 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
 // LSE merge of the n_split partials of the R_loc local rows of (b, g), D = 128:
 // lse = log2 sum_s 2^lse_s, o = sum_s 2^(lse_s - lse) o_s (empty splits drop out).
 __device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int R_loc) {
+  const auto ro = partial_rsrc(a.part_o);
+  const auto rl = partial_rsrc(a.part_lse);
   for (int e = threadIdx.x; e < R_loc * 32; e += blockDim.x) {
     const int r = e >> 5, d4 = (e & 31) * 4;
     const size_t row = out_row(a, b, g, r);
-    const float *pl = a.part_lse + row * a.n_split;
+    const size_t lbase = row * a.n_split * 4;
     float M = -INFINITY;
-    for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, pl[s]);
+    for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, partial_load1(rl, lbase + 4 * s));
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
     float lse = -INFINITY;
     if (M != -INFINITY) {
       float tot = 0.f;
-      const float *po = a.part_o + row * a.n_split * 128 + d4;
+      const size_t obase = (row * a.n_split * 128 + d4) * 4;
       for (int s = 0; s < a.n_split; ++s) {
-        const float w = exp2f(pl[s] - M);
+        const float w = exp2f(partial_load1(rl, lbase + 4 * s) - M);
         if (w == 0.f) continue;
-        const float4 v = *reinterpret_cast<const float4 *>(po + (size_t)s * 128);
+        const float4 v = partial_load4(ro, obase + (size_t)s * 512);
         tot += w;
         o.x = fmaf(w, v.x, o.x);
         o.y = fmaf(w, v.y, o.y);

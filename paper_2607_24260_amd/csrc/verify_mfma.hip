@@ -71,33 +71,28 @@ __device__ __forceinline__ u32x2 fp8x4_to_bf16x4(uint32_t w) {
   return u32x2{pack_bf16_exact(f0.x, f0.y), pack_bf16_exact(f1.x, f1.y)};
 }
 
+constexpr int kTileBytes(int kv) { return (kv == kBF16 ? 2 : 1) * kPage * kD; }
+
 // K tile operand of one page for k-block kb: key n, dims 32kb + 8j .. +7
+// (chunk 4kb + j of the page's chunk-major K tile)
 template <int KV>
-__device__ __forceinline__ u32x4 load_k(const AttnArgs &a, int page, int g, int n, int j, int kb) {
+__device__ __forceinline__ u32x4 load_k(__amdgpu_buffer_rsrc_t r, int n, int j, int kb) {
   if constexpr (KV == kBF16) {
-    const uint16_t *p = static_cast<const uint16_t *>(a.k_pages) +
-                        ((size_t)page * a.Hkv + g) * (kPage * kD) + (kb * 4 + j) * 128 + n * 8;
-    return load_stream(reinterpret_cast<const u32x4 *>(p));
+    return tile_load16(r, kb * 1024 + j * 256 + n * 16);
   } else {
-    const uint8_t *p = static_cast<const uint8_t *>(a.k_pages) +
-                       ((size_t)page * a.Hkv + g) * (kPage * kD) + (kb * 4 + j) * 128 + n * 8;
-    const u32x2 w = load_stream(reinterpret_cast<const u32x2 *>(p));
+    const u32x2 w = tile_load8(r, kb * 512 + j * 128 + n * 8);
     const u32x2 lo = fp8x4_to_bf16x4(w[0]), hi = fp8x4_to_bf16x4(w[1]);
     return u32x4{lo[0], lo[1], hi[0], hi[1]};
   }
 }
 
-// V^T operand half: dim d, keys 4j .. 4j+3 of one page, as 2 dwords of bf16
+// V^T operand half: dim dt*16 + n, keys 4j .. 4j+3 of one page, as 2 dwords of bf16
 template <int KV>
-__device__ __forceinline__ u32x2 load_vt(const AttnArgs &a, int page, int g, int d, int j) {
+__device__ __forceinline__ u32x2 load_vt(__amdgpu_buffer_rsrc_t r, int n, int j, int dt) {
   if constexpr (KV == kBF16) {
-    const uint16_t *p = static_cast<const uint16_t *>(a.v_pages) +
-                        ((size_t)page * a.Hkv + g) * (kPage * kD) + d * kPage + j * 4;
-    return load_stream(reinterpret_cast<const u32x2 *>(p));
+    return tile_load8(r, dt * 512 + n * 32 + j * 8);
   } else {
-    const uint8_t *p = static_cast<const uint8_t *>(a.v_pages) +
-                       ((size_t)page * a.Hkv + g) * (kPage * kD) + d * kPage + j * 4;
-    return fp8x4_to_bf16x4(load_stream(reinterpret_cast<const uint32_t *>(p)));
+    return fp8x4_to_bf16x4(tile_load4(r, dt * 256 + n * 16 + j * 4));
   }
 }
 
@@ -121,15 +116,20 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, co
   r.okB = pb >= 0 && (int64_t)pb < a.num_pages;
   r.pA = r.okA ? pa : 0;
   r.pB = r.okB ? pb : r.pA;
+  const size_t tile = kTileBytes(KV);
+  const auto kra = tile_rsrc(a.k_pages, ((size_t)r.pA * a.Hkv + g) * tile, (int)tile);
+  const auto krb = tile_rsrc(a.k_pages, ((size_t)r.pB * a.Hkv + g) * tile, (int)tile);
+  const auto vra = tile_rsrc(a.v_pages, ((size_t)r.pA * a.Hkv + g) * tile, (int)tile);
+  const auto vrb = tile_rsrc(a.v_pages, ((size_t)r.pB * a.Hkv + g) * tile, (int)tile);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
-    r.kA[kb] = load_k<KV>(a, r.pA, g, n, j, kb);
-    r.kB[kb] = load_k<KV>(a, r.pB, g, n, j, kb);
+    r.kA[kb] = load_k<KV>(kra, n, j, kb);
+    r.kB[kb] = load_k<KV>(krb, n, j, kb);
   }
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) {
-    r.vA[dt] = load_vt<KV>(a, r.pA, g, dt * 16 + n, j);
-    r.vB[dt] = load_vt<KV>(a, r.pB, g, dt * 16 + n, j);
+    r.vA[dt] = load_vt<KV>(vra, n, j, dt);
+    r.vB[dt] = load_vt<KV>(vrb, n, j, dt);
   }
 }
 
@@ -382,6 +382,8 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
     __syncthreads();
     // wavefront 0 writes the tile (final output, or this split's partial)
     if (threadIdx.x < 64) {
+      const auto ro = partial_rsrc(a.part_o);
+      const auto rl = partial_rsrc(a.part_lse);
 #pragma unroll
       for (int t8 = 0; t8 < 8; ++t8) {
         const int f = threadIdx.x + 64 * t8;      // float4 index in [16][128]
@@ -389,15 +391,17 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
         const int r = nt * 16 + rr;
         if (r < R) {
           const size_t row = out_row(a, b, g, r);
-          float *dst = (a.n_split == 1) ? a.out + row * kD + d4
-                                        : a.part_o + (row * a.n_split + split) * kD + d4;
-          *reinterpret_cast<float4 *>(dst) = *reinterpret_cast<const float4 *>(&s_out[rr][d4]);
+          const float4 v = *reinterpret_cast<const float4 *>(&s_out[rr][d4]);
+          if (a.n_split == 1)
+            *reinterpret_cast<float4 *>(a.out + row * kD + d4) = v;
+          else
+            partial_store4(ro, ((row * a.n_split + split) * kD + d4) * 4, v);
         }
       }
       if (threadIdx.x < 16 && nt * 16 + threadIdx.x < R) {
         const size_t row = out_row(a, b, g, nt * 16 + threadIdx.x);
         if (a.n_split == 1) a.lse[row] = s_olse[threadIdx.x] * kLn2;
-        else a.part_lse[row * a.n_split + split] = s_olse[threadIdx.x];
+        else partial_store1(rl, (row * a.n_split + split) * 4, s_olse[threadIdx.x]);
       }
     }
     __syncthreads();
