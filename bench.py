@@ -64,6 +64,37 @@ def plan_bytes(w, view_blocks):
             + int(np.sum(view_blocks)) * 8 + B * 16)
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "kap_128k_5p5pct_hbm_traffic.txt")
+KERNEL_SOURCES = {
+    "verify_mfma_kernel": ["paper_2607_24260_amd/csrc/verify_mfma.hip",
+                           "paper_2607_24260_amd/csrc/kap_internal.h"],
+    "decode_fast_kernel": ["paper_2607_24260_amd/csrc/decode_fast.hip",
+                           "paper_2607_24260_amd/csrc/kap_internal.h"],
+}
+
+
+def counter_traffic(kernel):
+    """HBM bytes per dispatch of `kernel` from the committed rocprofv3 counter
+    summary, or None when the kernel's sources changed since the counters were
+    taken (or the summary is missing)."""
+    import hashlib
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return None
+    vals = {}
+    for ln in lines:
+        parts = ln.split()
+        if len(parts) == 4 and parts[2] == "=" and parts[1] == kernel:
+            vals[parts[0]] = parts[3]
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    if vals.get("source_sha256") != h.hexdigest() or "traffic_bytes" not in vals:
+        return None
+    return int(vals["traffic_bytes"])
+
+
 def time_loop(fn, n, reps, torch):
     """Median over `reps` of the mean time per call of `n` back-to-back calls,
     bracketed by HIP events on the current stream."""
@@ -139,6 +170,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--profile", action="store_true",
                     help="only the timed steps (for rocprofv3 runs)")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="also run a 1 GiB device-to-device copy (known bytes for scaling "
+                         "FETCH_SIZE / WRITE_SIZE counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -236,6 +270,14 @@ def main():
     ver_b = algorithmic_bytes(w, view_tokens, view_blocks, "verify", q_len)
     step_b = plan_bytes(w, view_blocks) + n_dec * dec_b + n_ver * ver_b
 
+    if args.calibrate:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     for _ in range(args.warmup):
         step(0)
     torch.cuda.synchronize()
@@ -305,12 +347,14 @@ def main():
         "roofline": {
             "kernel": "kap_verify (verify_mfma_kernel, splits merged in-kernel)",
             "bound": "hbm", "achieved": round(ver_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(ver_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(ver_gbs / HBM_PEAK_GBS, 4),
+            "traffic": counter_traffic("verify_mfma_kernel") if cfg == 4 else None,
         },
         "decode_roofline": {
             "kernel": "kap_selected_decode (decode_fast_kernel, splits merged in-kernel)",
             "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+            "traffic": counter_traffic("decode_fast_kernel") if cfg == 4 else None,
         },
         "cpu_baseline": cpu,
     }

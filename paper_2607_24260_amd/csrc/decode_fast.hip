@@ -77,14 +77,18 @@ template <int KV> struct PageRegs;
 template <> struct PageRegs<kBF16> { u32x4 k[4]; u32x4 v[4]; };
 template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x2 v[4]; };
 
+// Loads of one (page, head) tile. With live == false the descriptor covers
+// zero bytes: the loads return zeros without touching memory (used for
+// invalid pages and for the ring's prefetches past a wavefront's last page).
 template <int KV>
 __device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, int page, int g,
-                                          int lane) {
+                                          int lane, bool live) {
   const int t = lane >> 2, c = lane & 3;
   constexpr int kTile = (KV == kBF16 ? 2 : 1) * kPage * kD;   // bytes per (page, head) tile
   const size_t off = ((size_t)page * a.Hkv + g) * kTile;
-  const auto kr = tile_rsrc(a.k_pages, off, kTile);
-  const auto vr = tile_rsrc(a.v_pages, off, kTile);
+  const int bytes = live ? kTile : 0;
+  const auto kr = tile_rsrc(a.k_pages, off, bytes);
+  const auto vr = tile_rsrc(a.v_pages, off, bytes);
   if constexpr (KV == kBF16) {
     // K: chunk 4i + c of token t; V^T: 1 KB row block i, 16 bytes per lane
 #pragma unroll
@@ -191,14 +195,18 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[hh][i] = 0.f;
 
-  // View block kk of this wavefront -> a page that is safe to read (page 0
-  // stands in for an invalid id) and its number of visible tokens (0 if the
-  // id is invalid or the block lies past the sequence).
-  auto page_info = [&](int kk, int &page, int &nvalid) {
+  const int kw = k0 + wave;
+  const int n_my = kw < k1 ? (k1 - kw + kWaves - 1) / kWaves : 0;
+
+  // The i-th view block of this wavefront -> its page (0 for an invalid id)
+  // and number of visible tokens (0 if the id is invalid, the block lies past
+  // the sequence, or i is past this wavefront's blocks).
+  auto page_info = [&](int i, int &page, int &nvalid) {
+    const int kk = kw + kWaves * min(i, n_my - 1);
     page = vbt[kk];
     const long long rem = (long long)L - (long long)vlb[kk] * kPage;
     nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
-    if (page < 0 || (int64_t)page >= a.num_pages) {
+    if (page < 0 || (int64_t)page >= a.num_pages || i >= n_my) {
       nvalid = 0;
       page = 0;
     }
@@ -288,33 +296,29 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 
   // Three page buffers, unrolled by three: while one page is processed the
   // loads of the next two are in flight. Loads are unconditional (past the end
-  // of this wavefront's pages the last page is re-read, an L2 hit) so the
-  // steady state is straight-line code and only the oldest buffer's loads are
-  // waited for.
-  const int kw = k0 + wave;
-  const int n_my = kw < k1 ? (k1 - kw + kWaves - 1) / kWaves : 0;
+  // of this wavefront's pages they go through an empty descriptor and read
+  // nothing), so the steady state is straight-line code.
   if (n_my > 0) {
-    auto kidx = [&](int i) { return kw + kWaves * min(i, n_my - 1); };
     PageRegs<KV> ra, rb, rc;
     int pga, nva, pgb, nvb, pgc, nvc;
-    page_info(kidx(0), pga, nva);
-    load_page<KV>(ra, a, pga, g, lane);
-    page_info(kidx(1), pgb, nvb);
-    load_page<KV>(rb, a, pgb, g, lane);
-    page_info(kidx(2), pgc, nvc);
-    load_page<KV>(rc, a, pgc, g, lane);
+    page_info(0, pga, nva);
+    load_page<KV>(ra, a, pga, g, lane, nva > 0);
+    page_info(1, pgb, nvb);
+    load_page<KV>(rb, a, pgb, g, lane, nvb > 0);
+    page_info(2, pgc, nvc);
+    load_page<KV>(rc, a, pgc, g, lane, nvc > 0);
     for (int i = 0; i < n_my; i += 3) {
       process(ra, pga, nva);
-      page_info(kidx(i + 3), pga, nva);
-      load_page<KV>(ra, a, pga, g, lane);
+      page_info(i + 3, pga, nva);
+      load_page<KV>(ra, a, pga, g, lane, nva > 0);
       if (i + 1 >= n_my) break;
       process(rb, pgb, nvb);
-      page_info(kidx(i + 4), pgb, nvb);
-      load_page<KV>(rb, a, pgb, g, lane);
+      page_info(i + 4, pgb, nvb);
+      load_page<KV>(rb, a, pgb, g, lane, nvb > 0);
       if (i + 2 >= n_my) break;
       process(rc, pgc, nvc);
-      page_info(kidx(i + 5), pgc, nvc);
-      load_page<KV>(rc, a, pgc, g, lane);
+      page_info(i + 5, pgc, nvc);
+      load_page<KV>(rc, a, pgc, g, lane, nvc > 0);
     }
   }
 

@@ -105,22 +105,24 @@ struct PairRegs {
   bool okA, okB;
 };
 
-// Pair at pages k, k+1 (k + 1 may lie past the sequence). Invalid page ids
-// read page 0 and are masked by value, so every load is unconditional.
+// Pair at pages k, k+1 (k + 1 may lie past the sequence). Missing or invalid
+// pages, and pairs past the wavefront's share (live == false), load through a
+// zero-byte descriptor: zeros, no memory traffic, and no branches.
 template <int KV>
 __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, const int32_t *fbt,
-                                          int k, int k_end, int g, int n, int j) {
+                                          int k, int k_end, int g, int n, int j, bool live) {
   const int pa = fbt[k];
   const int pb = (k + 1 < k_end) ? fbt[k + 1] : -1;
-  r.okA = pa >= 0 && (int64_t)pa < a.num_pages;
-  r.okB = pb >= 0 && (int64_t)pb < a.num_pages;
+  r.okA = live && pa >= 0 && (int64_t)pa < a.num_pages;
+  r.okB = live && pb >= 0 && (int64_t)pb < a.num_pages;
   r.pA = r.okA ? pa : 0;
-  r.pB = r.okB ? pb : r.pA;
+  r.pB = r.okB ? pb : 0;
   const size_t tile = kTileBytes(KV);
-  const auto kra = tile_rsrc(a.k_pages, ((size_t)r.pA * a.Hkv + g) * tile, (int)tile);
-  const auto krb = tile_rsrc(a.k_pages, ((size_t)r.pB * a.Hkv + g) * tile, (int)tile);
-  const auto vra = tile_rsrc(a.v_pages, ((size_t)r.pA * a.Hkv + g) * tile, (int)tile);
-  const auto vrb = tile_rsrc(a.v_pages, ((size_t)r.pB * a.Hkv + g) * tile, (int)tile);
+  const int ba = r.okA ? (int)tile : 0, bb = r.okB ? (int)tile : 0;
+  const auto kra = tile_rsrc(a.k_pages, ((size_t)r.pA * a.Hkv + g) * tile, ba);
+  const auto krb = tile_rsrc(a.k_pages, ((size_t)r.pB * a.Hkv + g) * tile, bb);
+  const auto vra = tile_rsrc(a.v_pages, ((size_t)r.pA * a.Hkv + g) * tile, ba);
+  const auto vrb = tile_rsrc(a.v_pages, ((size_t)r.pB * a.Hkv + g) * tile, bb);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     r.kA[kb] = load_k<KV>(kra, n, j, kb);
@@ -191,9 +193,9 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
   // Three pair buffers (two for 9..12-token windows, one beyond), unrolled:
-  // while one pair is processed the loads of the next ones are in flight. Past the end of this wavefront's
-  // pairs the last pair is re-read (an L2 hit), so the steady state is
-  // straight-line code and only the oldest buffer's loads are waited for.
+  // while one pair is processed the loads of the next ones are in flight.
+  // Past the end of this wavefront's pairs the loads go through an empty
+  // descriptor (no traffic), so the steady state is straight-line code.
   auto process = [&](PairRegs<KV> &P, int k) {
 
     float kscA = a.scale_log2, kscB = a.scale_log2, vscA = 1.f, vscB = 1.f;
@@ -305,35 +307,35 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
     auto kpair = [&](int i) { return 2 * (qw + kVerifyWaves * min(i, n_my - 1)); };
     if constexpr (NT <= 2) {
       PairRegs<KV> ra, rb, rc;
-      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j);
-      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j);
-      load_pair<KV>(rc, a, fbt, kpair(2), np_seq, g, n, j);
+      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j, (0) < n_my);
+      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j, (1) < n_my);
+      load_pair<KV>(rc, a, fbt, kpair(2), np_seq, g, n, j, (2) < n_my);
       for (int i = 0; i < n_my; i += 3) {
         process(ra, kpair(i));
-        load_pair<KV>(ra, a, fbt, kpair(i + 3), np_seq, g, n, j);
+        load_pair<KV>(ra, a, fbt, kpair(i + 3), np_seq, g, n, j, (i + 3) < n_my);
         if (i + 1 >= n_my) break;
         process(rb, kpair(i + 1));
-        load_pair<KV>(rb, a, fbt, kpair(i + 4), np_seq, g, n, j);
+        load_pair<KV>(rb, a, fbt, kpair(i + 4), np_seq, g, n, j, (i + 4) < n_my);
         if (i + 2 >= n_my) break;
         process(rc, kpair(i + 2));
-        load_pair<KV>(rc, a, fbt, kpair(i + 5), np_seq, g, n, j);
+        load_pair<KV>(rc, a, fbt, kpair(i + 5), np_seq, g, n, j, (i + 5) < n_my);
       }
     } else if constexpr (NT == 4) {   // 13..16-token windows: one buffer
       PairRegs<KV> ra;
       for (int i = 0; i < n_my; ++i) {
-        load_pair<KV>(ra, a, fbt, kpair(i), np_seq, g, n, j);
+        load_pair<KV>(ra, a, fbt, kpair(i), np_seq, g, n, j, (i) < n_my);
         process(ra, kpair(i));
       }
     } else {   // 9..12-token windows hold more accumulators: two buffers
       PairRegs<KV> ra, rb;
-      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j);
-      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j);
+      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j, (0) < n_my);
+      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j, (1) < n_my);
       for (int i = 0; i < n_my; i += 2) {
         process(ra, kpair(i));
-        load_pair<KV>(ra, a, fbt, kpair(i + 2), np_seq, g, n, j);
+        load_pair<KV>(ra, a, fbt, kpair(i + 2), np_seq, g, n, j, (i + 2) < n_my);
         if (i + 1 >= n_my) break;
         process(rb, kpair(i + 1));
-        load_pair<KV>(rb, a, fbt, kpair(i + 3), np_seq, g, n, j);
+        load_pair<KV>(rb, a, fbt, kpair(i + 3), np_seq, g, n, j, (i + 3) < n_my);
       }
     }
   }
