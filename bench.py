@@ -110,11 +110,11 @@ def time_loop(fn, n, reps, torch):
     return statistics.median(out)
 
 
-def cpu_baseline(w, plans_view, budget_s=20.0):
+def cpu_baseline(w, budget_s=12.0):
     """The fp64 oracle on the host cores, on a bounded sample of the workload:
-    one plan compile, one selected-view decode step over the whole batch and
-    verify of sequence 0 (all KV heads) for one call. Rate = algorithmic bytes
-    of that sample / wall time."""
+    one plan compile, then the step's schedule in order (a decode call over the
+    whole batch, or a verify call over the whole batch) until `budget_s` seconds
+    of work are done. Rate = algorithmic bytes of the calls done / wall time."""
     from oracle import kap_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -134,27 +134,31 @@ def cpu_baseline(w, plans_view, budget_s=20.0):
         vbt[b, :p.num_blocks] = p.block_table
         vlb[b, :p.num_blocks] = p.logical_blocks
     nb = [p.num_blocks for p in plans]
-    t0 = time.perf_counter()
-    O.selected_decode(pool, w.q_decode[0].float().cpu().numpy(), w.seq_lens, vbt, vlb, nb,
-                      w.sm_scale)
-    t_dec = time.perf_counter() - t0
-    qv = w.q_verify[0].float().cpu().numpy()
-    t0 = time.perf_counter()
-    O.verify(pool, qv, w.seq_lens, w.full_block_table, w.sm_scale, batches=[0])
-    t_ver = time.perf_counter() - t0
     vt = [p.view_tokens for p in plans]
-    dec_bytes = algorithmic_bytes(w, vt, nb, "decode")
-    per_tok = BYTES_PER_TOKEN[w.kv_dtype]
-    ver_bytes = int(w.seq_lens[0]) * per_tok
-    total = dec_bytes + ver_bytes
-    secs = t_plan + t_dec + t_ver
+    total = plan_bytes(w, nb)
+    done = {"decode": 0, "verify": 0}
+    secs = t_plan
+    for kind, i in w.schedule:
+        t0 = time.perf_counter()
+        if kind == "decode":
+            O.selected_decode(pool, w.q_decode[i].float().cpu().numpy(), w.seq_lens, vbt, vlb,
+                              nb, w.sm_scale)
+            total += algorithmic_bytes(w, vt, nb, "decode")
+        else:
+            qv = w.q_verify[i].float().cpu().numpy()
+            O.verify(pool, qv, w.seq_lens, w.full_block_table, w.sm_scale)
+            total += algorithmic_bytes(w, vt, nb, "verify", qv.shape[1])
+        secs += time.perf_counter() - t0
+        done[kind] += 1
+        if secs >= budget_s:
+            break
     aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     return {
         "value": round(total / secs / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": (f"1 plan compile ({t_plan:.2f}s) + 1 selected-view decode step over all "
-                   f"{w.batch} sequences ({t_dec:.2f}s) + verify of sequence 0, all KV heads, "
-                   f"q_len={qv.shape[1]} ({t_ver:.2f}s); fp64 numpy"),
+        "sample": (f"1 plan compile ({t_plan:.2f}s), then the step's schedule in order until "
+                   f"{budget_s:.0f}s: {done['decode']} decode calls and {done['verify']} verify "
+                   f"calls over all {w.batch} sequences; fp64 numpy"),
         "seconds": round(secs, 3),
         "host_cpus": os.cpu_count(), "affinity_cpus": aff, "blas_threads": blas_threads,
     }
@@ -308,7 +312,7 @@ def main():
 
     cpu = None
     if not args.no_cpu:
-        cpu = cpu_baseline(w, None)
+        cpu = cpu_baseline(w)
         log(f"cpu oracle: {cpu}")
 
     res = {

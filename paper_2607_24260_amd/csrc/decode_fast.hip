@@ -2,10 +2,10 @@
 // query heads per KV head -- the proposal step of Sec. 3.2 of the paper.
 //
 // Work decomposition: one 256-thread workgroup per (key split, KV head,
-// sequence); split s of n takes view pages [s*nb/n, (s+1)*nb/n) of the
-// sequence's actual view length nb. Its four wavefronts take those pages
-// round-robin (the next two pages' loads in flight while one is processed), keep
-// their own online-softmax state, and merge through LDS at the end. With more than one
+// sequence). The 4 n wavefronts of the n splits of (sequence, KV head) take the
+// view's nb entries round-robin (an even share of the actual view), keep the
+// next pages' loads in flight while one is processed, keep their own
+// online-softmax state, and merge through LDS at the end of the workgroup. With more than one
 // split the workgroup writes a partial (o, lse); the workgroup that finishes
 // last for its (sequence, KV head) merges all splits (atomic arrival counter
 // in the workspace), so one launch produces the final output.
@@ -35,6 +35,15 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kD = 128;
 constexpr int kWaves = 4;
+// pages in flight per wavefront (register ring depth)
+#ifndef KAP_DECODE_RING_BF16
+#define KAP_DECODE_RING_BF16 3
+#endif
+#ifndef KAP_DECODE_RING_FP8
+#define KAP_DECODE_RING_FP8 3
+#endif
+constexpr int kRingBF16 = KAP_DECODE_RING_BF16;
+constexpr int kRingFP8 = KAP_DECODE_RING_FP8;
 
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
@@ -148,7 +157,7 @@ __device__ __forceinline__ void v_floats(const PageRegs<KV> &r, float vv[4][8]) 
   }
 }
 
-template <int KV>
+template <int KV, int RING>
 __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   __shared__ float pbuf[kWaves][64];
   __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
@@ -167,11 +176,25 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   const int L = a.seq_lens[b];
   int nb = a.num_blocks[b];
   nb = max(0, min(nb, a.max_blocks));
-  // split `split` of n_split takes an even share of this sequence's view
-  const int k0 = (int)(((long long)split * nb) / a.n_split);
-  const int k1 = (int)(((long long)(split + 1) * nb) / a.n_split);
+  // The n_split * 4 wavefronts of (b, g) take the view's entries round-robin:
+  // wavefront u = 4 * split + wave takes entries u, u + nw, u + 2 nw, ...
+  // (an even share of the actual view, within one page). Table reads are
+  // clamped to the row, not to the view, so they need not wait for nb.
+  const int nw = a.n_split * kWaves;
+  const int u = split * kWaves + wave;
+  // (With max_blocks == 0 the host points both tables at seq_lens with row
+  // stride 0, so entry 0 of the row is always readable.)
   const int32_t *vbt = a.block_table + (size_t)b * a.bt_stride;
   const int32_t *vlb = a.logical_block + (size_t)b * a.bt_stride;
+  const int last_entry = max(a.max_blocks - 1, 0);
+  auto table_read = [&](int i, int &raw_page, int &raw_lblk) {
+    const int kk = min(u + nw * i, last_entry);
+    raw_page = vbt[kk];
+    raw_lblk = vlb[kk];
+  };
+  int raw_pg[RING], raw_lb[RING];
+#pragma unroll
+  for (int j = 0; j < RING; ++j) table_read(j, raw_pg[j], raw_lb[j]);
 
   // query slices of the four heads, as bf16 pairs matching the K slice
   uint32_t qr[4][4][4];
@@ -195,21 +218,24 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[hh][i] = 0.f;
 
-  const int kw = k0 + wave;
-  const int n_my = kw < k1 ? (k1 - kw + kWaves - 1) / kWaves : 0;
+  const int n_my = u < nb ? (nb - 1 - u) / nw + 1 : 0;
 
-  // The i-th view block of this wavefront -> its page (0 for an invalid id)
+  // The i-th view entry of this wavefront -> its page (0 for an invalid id)
   // and number of visible tokens (0 if the id is invalid, the block lies past
-  // the sequence, or i is past this wavefront's blocks).
-  auto page_info = [&](int i, int &page, int &nvalid) {
-    const int kk = kw + kWaves * min(i, n_my - 1);
-    page = vbt[kk];
-    const long long rem = (long long)L - (long long)vlb[kk] * kPage;
+  // the sequence, or i is past this wavefront's entries).
+  auto validate = [&](int i, int raw_page, int raw_lblk, int &page, int &nvalid) {
+    const long long rem = (long long)L - (long long)raw_lblk * kPage;
     nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
+    page = raw_page;
     if (page < 0 || (int64_t)page >= a.num_pages || i >= n_my) {
       nvalid = 0;
       page = 0;
     }
+  };
+  auto page_info = [&](int i, int &page, int &nvalid) {   // used only when n_my > 0
+    int rp, rl;
+    table_read(i, rp, rl);
+    validate(i, rp, rl, page, nvalid);
   };
 
   auto process = [&](const PageRegs<KV> &cur, int page, int nvalid) {
@@ -294,33 +320,32 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
 
-  // Three page buffers, unrolled by three: while one page is processed the
-  // loads of the next two are in flight. Loads are unconditional (past the end
+  // RING page buffers, unrolled by RING: while one page is processed the loads
+  // of the next RING - 1 are in flight. Loads are unconditional (past the end
   // of this wavefront's pages they go through an empty descriptor and read
-  // nothing), so the steady state is straight-line code.
-  if (n_my > 0) {
-    PageRegs<KV> ra, rb, rc;
-    int pga, nva, pgb, nvb, pgc, nvc;
-    page_info(0, pga, nva);
-    load_page<KV>(ra, a, pga, g, lane, nva > 0);
-    page_info(1, pgb, nvb);
-    load_page<KV>(rb, a, pgb, g, lane, nvb > 0);
-    page_info(2, pgc, nvc);
-    load_page<KV>(rc, a, pgc, g, lane, nvc > 0);
-    for (int i = 0; i < n_my; i += 3) {
-      process(ra, pga, nva);
-      page_info(i + 3, pga, nva);
-      load_page<KV>(ra, a, pga, g, lane, nva > 0);
-      if (i + 1 >= n_my) break;
-      process(rb, pgb, nvb);
-      page_info(i + 4, pgb, nvb);
-      load_page<KV>(rb, a, pgb, g, lane, nvb > 0);
-      if (i + 2 >= n_my) break;
-      process(rc, pgc, nvc);
-      page_info(i + 5, pgc, nvc);
-      load_page<KV>(rc, a, pgc, g, lane, nvc > 0);
+  // nothing), so the steady state is straight-line code. The main loop runs
+  // whole rounds of RING pages with no early exit -- an exit inside the round
+  // would merge a just-issued load into the loop header's wait and drain the
+  // ring every round -- and the remaining pages are processed after it.
+  PageRegs<KV> r[RING];
+  int pg[RING], nv[RING];
+#pragma unroll
+  for (int j = 0; j < RING; ++j) {
+    validate(j, raw_pg[j], raw_lb[j], pg[j], nv[j]);
+    load_page<KV>(r[j], a, pg[j], g, lane, nv[j] > 0);
+  }
+  const int full = n_my - n_my % RING;
+  for (int i = 0; i < full; i += RING) {
+#pragma unroll
+    for (int j = 0; j < RING; ++j) {
+      process(r[j], pg[j], nv[j]);
+      page_info(i + j + RING, pg[j], nv[j]);
+      load_page<KV>(r[j], a, pg[j], g, lane, nv[j] > 0);
     }
   }
+#pragma unroll
+  for (int j = 0; j < RING - 1; ++j)
+    if (full + j < n_my) process(r[j], pg[j], nv[j]);
 
   // ---- per-wave totals -------------------------------------------------------
   float lt = l_c + dpp<kRowRor4>(l_c);
@@ -397,9 +422,9 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s) {
   const dim3 grid(a.n_split, a.Hkv, a.batch);
   if (a.kv_type == kBF16)
-    hipLaunchKernelGGL(decode_fast_kernel<kBF16>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((decode_fast_kernel<kBF16, kRingBF16>), grid, dim3(256), 0, s, a);
   else if (a.kv_type == kFP8)
-    hipLaunchKernelGGL(decode_fast_kernel<kFP8>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((decode_fast_kernel<kFP8, kRingFP8>), grid, dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -409,8 +434,8 @@ int decode_fast_blocks_per_cu(int kv_type) {
   int nb = 0;
   const hipError_t e =
       kv_type == kFP8
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kFP8>, 256, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kBF16>, 256, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kFP8, kRingFP8>, 256, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kBF16, kRingBF16>, 256, 0);
   return e == hipSuccess ? nb : 0;
 }
 

@@ -363,9 +363,13 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
   a.q_f32 = kv->q_dtype == KAP_DT_F32;
   a.q_len = 1;
   a.seq_lens = seq_lens;
-  a.block_table = view_block_table;
-  a.bt_stride = view_stride;
-  a.logical_block = view_logical_block;
+  // An empty view may come with NULL tables: point them at seq_lens (row
+  // stride 0) so kernels may read entry 0 of a row without a guard; no entry
+  // is used, since every view is then empty.
+  const bool no_table = max_view_blocks == 0;
+  a.block_table = no_table ? seq_lens : view_block_table;
+  a.bt_stride = no_table ? 0 : view_stride;
+  a.logical_block = no_table ? seq_lens : view_logical_block;
   a.num_blocks = view_num_blocks;
   a.max_blocks = max_view_blocks;
   a.causal = 0;

@@ -216,30 +216,51 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
 
 // LSE merge of the n_split partials of the R_loc local rows of (b, g), D = 128:
 // lse = log2 sum_s 2^lse_s, o = sum_s 2^(lse_s - lse) o_s (empty splits drop out).
+// The partials are read eight splits at a time with independent loads (one
+// memory round trip per eight splits) and folded in with a running maximum.
 __device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int R_loc) {
+  constexpr int kBatch = 8;
   const auto ro = partial_rsrc(a.part_o);
   const auto rl = partial_rsrc(a.part_lse);
+  const int ns = a.n_split;
   for (int e = threadIdx.x; e < R_loc * 32; e += blockDim.x) {
     const int r = e >> 5, d4 = (e & 31) * 4;
     const size_t row = out_row(a, b, g, r);
-    const size_t lbase = row * a.n_split * 4;
-    float M = -INFINITY;
-    for (int s = 0; s < a.n_split; ++s) M = fmaxf(M, partial_load1(rl, lbase + 4 * s));
+    const size_t lbase = row * ns * 4;
+    const size_t obase = (row * ns * 128 + d4) * 4;
+    float M = -INFINITY, tot = 0.f;
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int s0 = 0; s0 < ns; s0 += kBatch) {
+      float ls[kBatch];
+      float4 vs[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int s = min(s0 + j, ns - 1);
+        ls[j] = partial_load1(rl, lbase + 4 * (size_t)s);
+        vs[j] = partial_load4(ro, obase + (size_t)s * 512);
+      }
+      float mc = M;
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j)
+        if (s0 + j < ns) mc = fmaxf(mc, ls[j]);
+      if (mc == -INFINITY) continue;                 // every split so far is empty
+      const float sc = exp2f(M - mc);                // 0 while M is still -inf
+      tot *= sc;
+      o.x *= sc; o.y *= sc; o.z *= sc; o.w *= sc;
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        if (s0 + j >= ns) continue;
+        const float w = exp2f(ls[j] - mc);
+        tot += w;
+        o.x = fmaf(w, vs[j].x, o.x);
+        o.y = fmaf(w, vs[j].y, o.y);
+        o.z = fmaf(w, vs[j].z, o.z);
+        o.w = fmaf(w, vs[j].w, o.w);
+      }
+      M = mc;
+    }
     float lse = -INFINITY;
     if (M != -INFINITY) {
-      float tot = 0.f;
-      const size_t obase = (row * a.n_split * 128 + d4) * 4;
-      for (int s = 0; s < a.n_split; ++s) {
-        const float w = exp2f(partial_load1(rl, lbase + 4 * s) - M);
-        if (w == 0.f) continue;
-        const float4 v = partial_load4(ro, obase + (size_t)s * 512);
-        tot += w;
-        o.x = fmaf(w, v.x, o.x);
-        o.y = fmaf(w, v.y, o.y);
-        o.z = fmaf(w, v.z, o.z);
-        o.w = fmaf(w, v.w, o.w);
-      }
       const float inv = 1.f / tot;
       o.x *= inv; o.y *= inv; o.z *= inv; o.w *= inv;
       lse = (M + log2f(tot)) * kLn2;

@@ -192,10 +192,10 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  // Three pair buffers (two for 9..12-token windows, one beyond), unrolled:
-  // while one pair is processed the loads of the next ones are in flight.
-  // Past the end of this wavefront's pairs the loads go through an empty
-  // descriptor (no traffic), so the steady state is straight-line code.
+  // RING pair buffers (three; two for 9..12-token windows, one beyond),
+  // unrolled: while one pair is processed the loads of the next ones are in
+  // flight. Past the end of this wavefront's pairs the loads go through an
+  // empty descriptor (no traffic), so the steady state is straight-line code.
   auto process = [&](PairRegs<KV> &P, int k) {
 
     float kscA = a.scale_log2, kscB = a.scale_log2, vscA = 1.f, vscB = 1.f;
@@ -305,37 +305,21 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   const int n_my = qw < q1 ? (q1 - qw + kVerifyWaves - 1) / kVerifyWaves : 0;
   if (n_my > 0) {
     auto kpair = [&](int i) { return 2 * (qw + kVerifyWaves * min(i, n_my - 1)); };
-    if constexpr (NT <= 2) {
-      PairRegs<KV> ra, rb, rc;
-      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j, (0) < n_my);
-      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j, (1) < n_my);
-      load_pair<KV>(rc, a, fbt, kpair(2), np_seq, g, n, j, (2) < n_my);
-      for (int i = 0; i < n_my; i += 3) {
-        process(ra, kpair(i));
-        load_pair<KV>(ra, a, fbt, kpair(i + 3), np_seq, g, n, j, (i + 3) < n_my);
-        if (i + 1 >= n_my) break;
-        process(rb, kpair(i + 1));
-        load_pair<KV>(rb, a, fbt, kpair(i + 4), np_seq, g, n, j, (i + 4) < n_my);
-        if (i + 2 >= n_my) break;
-        process(rc, kpair(i + 2));
-        load_pair<KV>(rc, a, fbt, kpair(i + 5), np_seq, g, n, j, (i + 5) < n_my);
-      }
-    } else if constexpr (NT == 4) {   // 13..16-token windows: one buffer
-      PairRegs<KV> ra;
-      for (int i = 0; i < n_my; ++i) {
-        load_pair<KV>(ra, a, fbt, kpair(i), np_seq, g, n, j, (i) < n_my);
-        process(ra, kpair(i));
-      }
-    } else {   // 9..12-token windows hold more accumulators: two buffers
-      PairRegs<KV> ra, rb;
-      load_pair<KV>(ra, a, fbt, kpair(0), np_seq, g, n, j, (0) < n_my);
-      load_pair<KV>(rb, a, fbt, kpair(1), np_seq, g, n, j, (1) < n_my);
-      for (int i = 0; i < n_my; i += 2) {
-        process(ra, kpair(i));
-        load_pair<KV>(ra, a, fbt, kpair(i + 2), np_seq, g, n, j, (i + 2) < n_my);
-        if (i + 1 >= n_my) break;
-        process(rb, kpair(i + 1));
-        load_pair<KV>(rb, a, fbt, kpair(i + 3), np_seq, g, n, j, (i + 3) < n_my);
+    // Every round issues all RING loads unconditionally and skips only the
+    // processing of pairs past the end: an early exit inside a round would
+    // make the loop header wait for the just-issued loads, draining the ring
+    // every round.
+    constexpr int RING = NT <= 2 ? 3 : (NT == 3 ? 2 : 1);
+    PairRegs<KV> rr[RING];
+#pragma unroll
+    for (int jr = 0; jr < RING; ++jr)
+      load_pair<KV>(rr[jr], a, fbt, kpair(jr), np_seq, g, n, j, jr < n_my);
+    for (int i = 0; i < n_my; i += RING) {
+#pragma unroll
+      for (int jr = 0; jr < RING; ++jr) {
+        if (i + jr < n_my) process(rr[jr], kpair(i + jr));
+        load_pair<KV>(rr[jr], a, fbt, kpair(i + jr + RING), np_seq, g, n, j,
+                      i + jr + RING < n_my);
       }
     }
   }
