@@ -181,8 +181,10 @@ size_t kap_compile_plan_workspace_bytes(int32_t batch, int32_t num_spans,
  *   q [batch][Hq][D] (q_dtype); view arrays [batch][view_stride] int32 with
  *   view_stride >= max_view_blocks; view_num_blocks, seq_lens [batch] int32;
  *   out [batch][Hq][D] float32; lse [batch][Hq] float32.
- * num_splits (host): 0 = automatic; n > 0 forces n key splits per
- * (sequence, KV head) (clamped to the number of view blocks).
+ * num_splits (host): 0 = automatic -- the tuned path then sizes the key
+ * splits of each (sequence, KV head) on the device from that sequence's
+ * actual view, so ragged batches stay balanced; n > 0 forces n key splits
+ * per (sequence, KV head) (clamped to max_view_blocks).
  * Passing the full block table as the view, with view_logical_block[b][j] = j
  * and view_num_blocks[b] = ceil(seq_lens[b]/16), is full-context decode.
  */

@@ -157,7 +157,7 @@ __device__ __forceinline__ void v_floats(const PageRegs<KV> &r, float vv[4][8]) 
   }
 }
 
-template <int KV, int RING>
+template <int KV, int RING, bool BALANCED>
 __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   __shared__ float pbuf[kWaves][64];
   __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
@@ -166,35 +166,77 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   __shared__ float s_plse[4];
   __shared__ int s_flag;
 
-  const int split = blockIdx.x;
-  const int g = blockIdx.y;
-  const int b = blockIdx.z;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int t = lane >> 2, c = lane & 3, hf = lane & 1;
 
-  const int L = a.seq_lens[b];
-  int nb = a.num_blocks[b];
-  nb = max(0, min(nb, a.max_blocks));
+  // Work unit. Balanced mode: the map needs the view lengths of the whole
+  // batch, so the first table entries are read for a guess while it is
+  // computed -- the even assignment, a.guess_splits splits per unit, which
+  // the map produces for equal views -- and read again if the map differs.
+  WorkItem wi;
+  if constexpr (BALANCED) {
+    const int ng = a.guess_splits;
+    const int w = blockIdx.x;
+    const int q = div_small(w, ng);
+    wi.n_split = ng;
+    wi.split = w - q * ng;
+    const int bq = div_small(q, a.Hkv);
+    wi.g = q - bq * a.Hkv;
+    wi.b = min(bq, a.batch - 1);
+  } else {
+    wi.split = blockIdx.x;
+    wi.g = blockIdx.y;
+    wi.b = blockIdx.z;
+    wi.n_split = a.n_split;
+    wi.slot0 = (blockIdx.z * a.Hkv + blockIdx.y) * a.n_split;
+  }
+
   // The n_split * 4 wavefronts of (b, g) take the view's entries round-robin:
   // wavefront u = 4 * split + wave takes entries u, u + nw, u + 2 nw, ...
   // (an even share of the actual view, within one page). Table reads are
-  // clamped to the row, not to the view, so they need not wait for nb.
-  const int nw = a.n_split * kWaves;
+  // clamped to the row, not to the view, so they need not wait for the view
+  // length. (With max_blocks == 0 the host points both tables at seq_lens
+  // with row stride 0, so entry 0 of the row is always readable.)
+  const int last_entry = max(a.max_blocks - 1, 0);
+  int raw_pg[RING], raw_lb[RING];
+  auto first_entries = [&](const WorkItem &x) {
+    const int32_t *bt = a.block_table + (size_t)x.b * a.bt_stride;
+    const int32_t *lb = a.logical_block + (size_t)x.b * a.bt_stride;
+#pragma unroll
+    for (int j = 0; j < RING; ++j) {
+      const int kk = min(x.split * kWaves + wave + x.n_split * kWaves * j, last_entry);
+      raw_pg[j] = bt[kk];
+      raw_lb[j] = lb[kk];
+    }
+  };
+  int L, nb;
+  if constexpr (BALANCED) {
+    // view pages of sequence bb (per KV head) decide its split count
+    auto load = [&](int bb) {
+      return SeqLoad{max(0, min(a.num_blocks[bb], a.max_blocks)), a.seq_lens[bb]};
+    };
+    const SeqLoad first = map_first_loads(a, load);
+    first_entries(wi);
+    const WorkItem guess = wi;
+    if (!ragged_map(a, load, first, blockIdx.x, wi, nb, L)) return;
+    if (wi.b != guess.b || wi.split != guess.split || wi.n_split != guess.n_split)
+      first_entries(wi);
+  } else {
+    first_entries(wi);
+    L = a.seq_lens[wi.b];
+    nb = max(0, min(a.num_blocks[wi.b], a.max_blocks));
+  }
+  const int split = wi.split, g = wi.g, b = wi.b, n_split = wi.n_split;
+  const int nw = n_split * kWaves;
   const int u = split * kWaves + wave;
-  // (With max_blocks == 0 the host points both tables at seq_lens with row
-  // stride 0, so entry 0 of the row is always readable.)
   const int32_t *vbt = a.block_table + (size_t)b * a.bt_stride;
   const int32_t *vlb = a.logical_block + (size_t)b * a.bt_stride;
-  const int last_entry = max(a.max_blocks - 1, 0);
   auto table_read = [&](int i, int &raw_page, int &raw_lblk) {
     const int kk = min(u + nw * i, last_entry);
     raw_page = vbt[kk];
     raw_lblk = vlb[kk];
   };
-  int raw_pg[RING], raw_lb[RING];
-#pragma unroll
-  for (int j = 0; j < RING; ++j) table_read(j, raw_pg[j], raw_lb[j]);
 
   // query slices of the four heads, as bf16 pairs matching the K slice
   uint32_t qr[4][4][4];
@@ -218,7 +260,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) acc[hh][i] = 0.f;
 
-  const int n_my = u < nb ? (nb - 1 - u) / nw + 1 : 0;
+  const int n_my = u < nb ? div_small(nb - 1 - u, nw) + 1 : 0;
 
   // The i-th view entry of this wavefront -> its page (0 for an invalid id)
   // and number of visible tokens (0 if the id is invalid, the block lies past
@@ -389,7 +431,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     o1v = n1 / den;
     lse2 = M + log2f(den);
   }
-  if (a.n_split == 1) {
+  if (n_split == 1) {
     *reinterpret_cast<float2 *>(a.out + row * kD + d0) = make_float2(o0, o1v);
     if ((threadIdx.x & 63) == 0) a.lse[row] = lse2 * kLn2;
     return;
@@ -406,36 +448,43 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     for (int t2 = 0; t2 < 2; ++t2) {
       const int f = threadIdx.x + 64 * t2;       // float4 index in [4][128]
       const int h4 = f >> 5, d4 = (f & 31) * 4;
-      const size_t pr = ((size_t)b * a.Hq + g * 4 + h4) * a.n_split + split;
+      const size_t pr = (size_t)(wi.slot0 + split) * 4 + h4;
       partial_store4(ro, (pr * kD + d4) * 4, *reinterpret_cast<const float4 *>(&s_part[h4][d4]));
     }
     if (threadIdx.x < 4) {
-      const size_t pr = ((size_t)b * a.Hq + g * 4 + threadIdx.x) * a.n_split + split;
+      const size_t pr = (size_t)(wi.slot0 + split) * 4 + threadIdx.x;
       partial_store1(rl, pr * 4, s_plse[threadIdx.x]);
     }
   }
-  if (last_arrival(a, b, g, &s_flag)) merge_rows(a, b, g, 4);
+  if (last_arrival(a, b, g, n_split, &s_flag)) merge_rows(a, b, g, 4, wi.slot0, n_split);
+}
+
+template <int KV, int RING>
+hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
+  if (a.ragged)
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, true>), dim3(a.n_split), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, false>), dim3(a.n_split, a.Hkv, a.batch),
+                       dim3(256), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_split, a.Hkv, a.batch);
-  if (a.kv_type == kBF16)
-    hipLaunchKernelGGL((decode_fast_kernel<kBF16, kRingBF16>), grid, dim3(256), 0, s, a);
-  else if (a.kv_type == kFP8)
-    hipLaunchKernelGGL((decode_fast_kernel<kFP8, kRingFP8>), grid, dim3(256), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (a.kv_type == kBF16) return launch_kv<kBF16, kRingBF16>(a, s);
+  if (a.kv_type == kFP8) return launch_kv<kFP8, kRingFP8>(a, s);
+  return hipErrorInvalidValue;
 }
 
 int decode_fast_blocks_per_cu(int kv_type) {
   int nb = 0;
   const hipError_t e =
       kv_type == kFP8
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kFP8, kRingFP8>, 256, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, decode_fast_kernel<kBF16, kRingBF16>, 256, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &nb, decode_fast_kernel<kFP8, kRingFP8, true>, 256, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &nb, decode_fast_kernel<kBF16, kRingBF16, true>, 256, 0);
   return e == hipSuccess ? nb : 0;
 }
 

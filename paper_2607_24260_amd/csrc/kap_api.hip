@@ -84,9 +84,27 @@ bool fast_geometry(const kap_kv_cache *kv) {
 
 struct SplitPlan {
   bool fast;
-  int n_split;
-  int pps;  // most pages any split of the generic path can get
+  bool ragged;    // tuned kernels: split counts balanced on the device
+  int n_split;    // splits per (sequence, KV head); balanced mode: workgroups launched
+  int pps;        // most pages any split of the generic path can get
+  int w_target;   // balanced mode: workgroups the work is spread over
+  int min_chunk;  // balanced mode: fewest work items per split
+  long long slots;  // tuned kernels: partial slots
 };
+
+// Balanced mode sizing: the work of a call is spread over about
+// kTargetPerCU workgroups per CU, and a split keeps at least kMinChunk* work
+// items (decode: view pages, one per wavefront and more; verify: page pairs).
+#ifndef KAP_DECODE_TARGET_PER_CU
+#define KAP_DECODE_TARGET_PER_CU 1
+#endif
+#ifndef KAP_VERIFY_TARGET_PER_CU
+#define KAP_VERIFY_TARGET_PER_CU 1
+#endif
+constexpr int kDecodeTargetPerCU = KAP_DECODE_TARGET_PER_CU;
+constexpr int kVerifyTargetPerCU = KAP_VERIFY_TARGET_PER_CU;
+constexpr int kMinChunkDecode = 16;
+constexpr int kMinChunkVerify = 8;
 
 int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
@@ -107,26 +125,33 @@ int blocks_per_cu(int id, int kv_type, int q_len) {
   return c > 0 ? c : 0;
 }
 
-// Decode (tuned path): about one (split, KV head, sequence) workgroup per
-// CU; each split keeps >= 4 view pages (one per wavefront). Generic path:
-// splits of at most kGenericPagesPerSplit pages.
+// Decode. Tuned path: with num_splits > 0, that many splits for every
+// (sequence, KV head); otherwise the balanced mode, where the kernel sizes
+// each sequence's splits from its view (about kDecodeTargetPerCU
+// workgroups per CU over the whole call) -- unless there are so many
+// (sequence, KV head) units that one split each already fills the device.
+// Generic path: splits of at most kGenericPagesPerSplit pages.
 SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num_splits) {
-  SplitPlan p{fast_geometry(kv), 1, 1};
+  SplitPlan p{fast_geometry(kv), false, 1, 1, 0, 0, 0};
   const int mb = max_blocks > 0 ? max_blocks : 1;
+  const long long units = (long long)batch * kv->num_kv_heads;
   if (p.fast) {
-    int n;
     if (num_splits > 0) {
-      n = num_splits;
+      // uniform: the same split count for every (sequence, KV head)
+      p.n_split = num_splits > mb ? mb : num_splits;
+      p.slots = units * p.n_split;
+    } else if (units >= 4LL * kDecodeTargetPerCU * device_cus()) {
+      p.n_split = 1;
+      p.slots = units;
     } else {
-      // one workgroup per CU: short splits pay more in fixed per-workgroup
-      // work (query load, combine, merge ticket) than extra occupancy returns
-      const long long work = (long long)batch * kv->num_kv_heads;
-      n = (int)((long long)device_cus() / (work > 0 ? work : 1));
-      n = n < cdiv(mb, 4) ? n : cdiv(mb, 4);
+      // balanced: split counts follow each sequence's actual view
+      p.ragged = true;
+      p.w_target = kDecodeTargetPerCU * device_cus();
+      p.min_chunk = kMinChunkDecode;
+      p.n_split = (int)((long long)kap::kUnevenFactor * p.w_target + units);
+      p.slots = p.n_split;
     }
-    n = n < 1 ? 1 : (n > mb ? mb : n);
-    p.n_split = n;
-    p.pps = cdiv(mb, n);
+    p.pps = cdiv(mb, p.n_split);
   } else {
     int n = cdiv(mb, kap::kGenericPagesPerSplit);
     if (num_splits > n) n = num_splits > mb ? mb : num_splits;
@@ -136,27 +161,34 @@ SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num
   return p;
 }
 
-// Verify (tuned path): as decode, in page pairs, >= 1 pair per wavefront.
+// Verify (tuned path): as decode, with page pairs as the work items.
 SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_pages, int num_splits) {
-  SplitPlan p{fast_geometry(kv) && q_len * 4 <= 64, 1, 1};
+  SplitPlan p{fast_geometry(kv) && q_len * 4 <= 64, false, 1, 1, 0, 0, 0};
   const int mp = max_pages > 0 ? max_pages : 1;
+  const long long units = (long long)batch * kv->num_kv_heads;
   if (p.fast) {
     const int pairs = cdiv(mp, 2);
-    int n;
     if (num_splits > 0) {
-      n = num_splits;
+      p.n_split = num_splits > pairs ? pairs : num_splits;
+      p.slots = units * p.n_split;
     } else {
       const int fp8 = kv->kv_dtype == KAP_DT_FP8_E4M3FN;
       const int nt = (q_len * 4 + 15) / 16;
       int bpc = blocks_per_cu(2 + 4 * fp8 + (nt - 1), fp8 ? kap::kFP8 : kap::kBF16, q_len);
       if (bpc <= 0) bpc = 1;
-      const long long work = (long long)batch * kv->num_kv_heads;
-      n = (int)((long long)bpc * device_cus() / (work > 0 ? work : 1));
-      n = n < cdiv(pairs, 4) ? n : cdiv(pairs, 4);
+      if (units >= 4LL * kVerifyTargetPerCU * bpc * device_cus()) {
+        p.n_split = 1;
+        p.slots = units;
+        p.pps = 2 * pairs;
+        return p;
+      }
+      p.ragged = true;
+      p.w_target = kVerifyTargetPerCU * bpc * device_cus();
+      p.min_chunk = kMinChunkVerify;
+      p.n_split = (int)((long long)kap::kUnevenFactor * p.w_target + units);
+      p.slots = p.n_split;
     }
-    n = n < 1 ? 1 : (n > pairs ? pairs : n);
-    p.n_split = n;
-    p.pps = 2 * cdiv(pairs, n);
+    p.pps = 2 * cdiv(pairs, p.n_split);
   } else {
     int n = cdiv(mp, kap::kGenericPagesPerSplit);
     if (num_splits > n) n = num_splits > mp ? mp : num_splits;
@@ -167,18 +199,27 @@ SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_page
 }
 
 // Workspace: [arrival counters, batch*Hkv int32][partial o][partial lse],
-// each part 256-byte aligned. Nothing when there is a single split.
+// each part 256-byte aligned. Generic path: nothing for a single split;
+// partials [rows][n_split]. Tuned kernels: partials by slot, [slot][q_len*4],
+// nothing when every (sequence, KV head) has a single uniform split.
 struct WsLayout {
   size_t tickets, part_o, part_lse, total;
 };
 
 WsLayout ws_layout(const kap_kv_cache *kv, int batch, int q_len, const SplitPlan &p) {
   WsLayout w{0, 0, 0, 0};
-  if (p.n_split <= 1 || batch <= 0) return w;
-  const size_t rows = (size_t)batch * q_len * kv->num_q_heads;
+  if (batch <= 0) return w;
+  size_t prow;   // partial rows (one per split and output row)
+  if (p.fast) {
+    if (!p.ragged && p.n_split <= 1) return w;
+    prow = (size_t)p.slots * q_len * 4;
+  } else {
+    if (p.n_split <= 1) return w;
+    prow = (size_t)batch * q_len * kv->num_q_heads * p.n_split;
+  }
   const size_t t = round_up((size_t)batch * kv->num_kv_heads * sizeof(int32_t), 256);
-  const size_t o = round_up(rows * p.n_split * kv->head_dim * sizeof(float), 256);
-  const size_t l = round_up(rows * p.n_split * sizeof(float), 256);
+  const size_t o = round_up(prow * kv->head_dim * sizeof(float), 256);
+  const size_t l = round_up(prow * sizeof(float), 256);
   w.tickets = 0;
   w.part_o = t;
   w.part_lse = t + o;
@@ -194,6 +235,14 @@ kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const Spli
                             bool decode, void *ws, hipStream_t s) {
   a.n_split = p.n_split;
   a.pages_per_split = p.pps;
+  a.ragged = p.ragged ? 1 : 0;
+  a.w_target = p.w_target;
+  a.min_chunk = p.min_chunk;
+  {
+    const long long units = (long long)a.batch * a.Hkv;
+    const long long ng = units > 0 ? p.w_target / units : 1;
+    a.guess_splits = ng > 1 ? (int)ng : 1;
+  }
   const WsLayout w = ws_layout(kv, a.batch, a.q_len, p);
   if (p.fast && w.total > 0x7fffffffULL)
     return fail(KAP_ERR_UNSUPPORTED, "split partials need %zu bytes (> 2 GiB); pass fewer splits",

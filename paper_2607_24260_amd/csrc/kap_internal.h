@@ -63,10 +63,20 @@ struct AttnArgs {
   int max_blocks;                // host bound on pages read per sequence
   int causal;                    // verify: row i sees positions < L - q_len + i + 1
   float scale_log2;              // sm_scale * log2(e)
-  int n_split;
+  int n_split;                   // splits per (sequence, KV head); balanced mode: workgroups
   int pages_per_split;
-  float *part_o;    // [batch * R][n_split][D]   (normalised partial outputs)
-  float *part_lse;  // [batch * R][n_split]      (log2-domain partial LSE)
+  // Tuned kernels, balanced mode (ragged != 0): split counts per sequence
+  // come from its actual work on the device (see ragged_map); blockIdx.x is
+  // the partial slot. Otherwise the grid is (n_split, Hkv, batch).
+  int ragged;
+  int w_target;                  // balanced mode: workgroups the work is spread over
+  int min_chunk;                 // balanced mode: fewest work items per split
+  int guess_splits;              // balanced mode: max(1, w_target / (batch * Hkv))
+  // Partials. Generic path: [batch * R][n_split][D] and [batch * R][n_split].
+  // Tuned kernels: by slot, [slot][R_loc][D] and [slot][R_loc], R_loc =
+  // q_len * 4 local rows; (sequence, KV head) owns slots slot0 .. slot0 + n - 1.
+  float *part_o;    // normalised partial outputs
+  float *part_lse;  // log2-domain partial LSE
   int32_t *tickets; // [batch][Hkv] arrival counters of the fused merge (zero between calls)
   float *out;       // [batch * R][D]
   float *lse;       // [batch * R]
@@ -157,6 +167,135 @@ __device__ __forceinline__ int wave_sum_i(int x) {
 }
 
 // ---------------------------------------------------------------------------
+// balanced work map of the tuned kernels
+// ---------------------------------------------------------------------------
+
+// One (sequence b, KV head g, split) work unit; the splits of (b, g) own
+// partial slots slot0 .. slot0 + n_split - 1.
+struct WorkItem {
+  int b, g, split, n_split, slot0;
+};
+
+// Wavefront-wide inclusive prefix sum / running maximum through DPP row
+// shifts and row broadcasts (no LDS round trips); lane 63 holds the total.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_or_zero(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROWS, 0xF, false);
+}
+__device__ __forceinline__ int wave_scan_add(int x) {
+  x += dpp_or_zero<0x111, 0xF>(x);   // row_shr:1
+  x += dpp_or_zero<0x112, 0xF>(x);   // row_shr:2
+  x += dpp_or_zero<0x114, 0xF>(x);   // row_shr:4
+  x += dpp_or_zero<0x118, 0xF>(x);   // row_shr:8
+  x += dpp_or_zero<0x142, 0xA>(x);   // row_bcast:15 into rows 1, 3
+  x += dpp_or_zero<0x143, 0xC>(x);   // row_bcast:31 into rows 2, 3
+  return x;
+}
+__device__ __forceinline__ int wave_scan_max(int x) {   // x >= 0
+  x = max(x, dpp_or_zero<0x111, 0xF>(x));
+  x = max(x, dpp_or_zero<0x112, 0xF>(x));
+  x = max(x, dpp_or_zero<0x114, 0xF>(x));
+  x = max(x, dpp_or_zero<0x118, 0xF>(x));
+  x = max(x, dpp_or_zero<0x142, 0xA>(x));
+  x = max(x, dpp_or_zero<0x143, 0xC>(x));
+  return x;
+}
+__device__ __forceinline__ int lane63(int x) { return __builtin_amdgcn_readlane(x, 63); }
+
+// floor(n / d) for 0 <= n < 2^31 and d >= 1. The quotient of two doubles is
+// correctly rounded, and for n < 2^53 rounding never reaches the next
+// integer, so truncating it is exact (shorter than the integer division
+// sequence).
+__device__ __forceinline__ int div_small(int n, int d) {
+  return (int)((double)n / (double)d);
+}
+
+// Balanced mode: sequence b holds load(b).items work items per KV head (decode:
+// view pages; verify: page pairs), counted up to 2^24 for sizing. With
+// T = Hkv * sum_b items_b, the chunk is C = max(min_chunk, T / w_target)
+// items when the sequences are even (the largest holds at most 5/4 of the
+// mean: one split per workgroup slot is then balanced), else
+// T / (kUnevenFactor * w_target) -- finer chunks, which the hardware
+// dispatcher spreads over the CUs as they free up. Every (b, g) gets
+// n_b = max(1, round(items_b / C)) splits; slots are numbered sequence-major,
+// then KV head, then split. Workgroup w takes slot w and returns false past
+// the last slot. The result is the same in every wavefront, which computes
+// it alone (two passes over the batch, 64 sequences per pass). The grid
+// needs kUnevenFactor * w_target + batch * Hkv workgroups at most.
+#ifndef KAP_UNEVEN_FACTOR
+#define KAP_UNEVEN_FACTOR 4
+#endif
+constexpr int kUnevenFactor = KAP_UNEVEN_FACTOR;
+constexpr int kMapItemCap = 1 << 24;
+
+// What the map reads per sequence: its work items and one more value the
+// caller wants for the sequence it is given (returned through aux_b).
+struct SeqLoad {
+  int items, aux;
+};
+
+// The loads of sequences 0..63 (one per lane), issued early by the caller so
+// that their wait does not cover loads issued after them.
+template <class Load>
+__device__ __forceinline__ SeqLoad map_first_loads(const AttnArgs &a, Load load) {
+  const int lane = threadIdx.x & 63;
+  SeqLoad first = load(min(lane, a.batch - 1));   // branch-free; batch >= 1
+  if (lane >= a.batch) first.items = 0;
+  return first;
+}
+
+template <class Load>
+__device__ __forceinline__ bool ragged_map(const AttnArgs &a, Load load, const SeqLoad &first,
+                                           int w, WorkItem &wi, int &items_b, int &aux_b) {
+  const int lane = threadIdx.x & 63;
+  int v0 = min(first.items, kMapItemCap);
+  long long tot = lane63(wave_scan_add(v0));
+  int mx = lane63(wave_scan_max(v0));
+  for (int b0 = 64; b0 < a.batch; b0 += 64) {
+    const int v = b0 + lane < a.batch ? min(load(b0 + lane).items, kMapItemCap) : 0;
+    tot += lane63(wave_scan_add(v));
+    mx = max(mx, lane63(wave_scan_max(v)));
+  }
+  const long long T = tot * a.Hkv;
+  const bool even = 4LL * mx * a.batch <= 5 * tot;
+  const int W = even ? a.w_target : kUnevenFactor * a.w_target;
+  // C = ceil(T / W) through a correctly rounded double quotient: it can come
+  // out below the exact ceiling only by less than W * 2^-52 slots' worth,
+  // which cannot lift the slot count past W + batch * Hkv
+  long long C = (long long)__builtin_ceil((double)T / (double)W);
+  if (C < a.min_chunk) C = a.min_chunk;
+  const int Ci = (int)(C < kMapItemCap ? C : kMapItemCap);
+  int base = 0;
+  for (int b0 = 0; b0 < a.batch; b0 += 64) {
+    const int b = b0 + lane;
+    const bool in = b < a.batch;
+    SeqLoad m = first;
+    if (b0 > 0) m = in ? load(b) : SeqLoad{0, 0};
+    const int v = min(m.items, kMapItemCap);
+    const int nb = in ? max(1, div_small(v + Ci / 2, Ci)) : 0;
+    const int cnt = nb * a.Hkv;
+    const int incl = wave_scan_add(cnt);
+    const int excl = incl - cnt;
+    const unsigned long long hit = __ballot(in && w >= base + excl && w < base + incl);
+    if (hit) {
+      const int l = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+      const int e = base + __builtin_amdgcn_readlane(excl, l);
+      wi.n_split = __builtin_amdgcn_readlane(nb, l);
+      wi.b = b0 + l;
+      const int off = w - e;
+      wi.g = div_small(off, wi.n_split);
+      wi.split = off - wi.g * wi.n_split;
+      wi.slot0 = w - wi.split;
+      items_b = __builtin_amdgcn_readlane(m.items, l);
+      aux_b = __builtin_amdgcn_readlane(m.aux, l);
+      return true;
+    }
+    base += lane63(incl);
+  }
+  return false;
+}
+
+// ---------------------------------------------------------------------------
 // fused split merge for the tuned kernels (four query heads per KV head)
 // ---------------------------------------------------------------------------
 
@@ -197,7 +336,8 @@ __device__ __forceinline__ float partial_load1(__amdgpu_buffer_rsrc_t r, size_t 
 // n_split partials of (b, g). Only wavefront 0 may have written this
 // workgroup's partial (with partial_store*): it waits until those stores are
 // complete, then takes a ticket. The last workgroup resets the counter.
-__device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, int *flag) {
+__device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, int n_split,
+                                             int *flag) {
   if (threadIdx.x < 64) {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores are complete
@@ -205,7 +345,7 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
     if (threadIdx.x == 0) {
       int32_t *ctr = a.tickets + (size_t)b * a.Hkv + g;
       const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int last = (prev == a.n_split - 1) ? 1 : 0;
+      const int last = (prev == n_split - 1) ? 1 : 0;
       if (last) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       *flag = last;
     }
@@ -214,20 +354,19 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
   return *flag != 0;
 }
 
-// LSE merge of the n_split partials of the R_loc local rows of (b, g), D = 128:
+// LSE merge of the ns partials (slots slot0 .. slot0 + ns - 1) of the R_loc
+// local rows of (b, g), D = 128:
 // lse = log2 sum_s 2^lse_s, o = sum_s 2^(lse_s - lse) o_s (empty splits drop out).
 // The partials are read eight splits at a time with independent loads (one
 // memory round trip per eight splits) and folded in with a running maximum.
-__device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int R_loc) {
+__device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int R_loc, int slot0,
+                                           int ns) {
   constexpr int kBatch = 8;
   const auto ro = partial_rsrc(a.part_o);
   const auto rl = partial_rsrc(a.part_lse);
-  const int ns = a.n_split;
   for (int e = threadIdx.x; e < R_loc * 32; e += blockDim.x) {
     const int r = e >> 5, d4 = (e & 31) * 4;
     const size_t row = out_row(a, b, g, r);
-    const size_t lbase = row * ns * 4;
-    const size_t obase = (row * ns * 128 + d4) * 4;
     float M = -INFINITY, tot = 0.f;
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int s0 = 0; s0 < ns; s0 += kBatch) {
@@ -235,9 +374,9 @@ __device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int 
       float4 vs[kBatch];
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
-        const int s = min(s0 + j, ns - 1);
-        ls[j] = partial_load1(rl, lbase + 4 * (size_t)s);
-        vs[j] = partial_load4(ro, obase + (size_t)s * 512);
+        const size_t pr = (size_t)(slot0 + min(s0 + j, ns - 1)) * R_loc + r;
+        ls[j] = partial_load1(rl, pr * 4);
+        vs[j] = partial_load4(ro, (pr * 128 + d4) * 4);
       }
       float mc = M;
 #pragma unroll

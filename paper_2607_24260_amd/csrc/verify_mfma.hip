@@ -146,22 +146,38 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   __shared__ float s_olse[16];
   __shared__ int s_flag;
 
-  const int split = blockIdx.x;
-  const int g = blockIdx.y;
-  const int b = blockIdx.z;
+  WorkItem wi;
+  int L;
+  if (a.ragged) {
+    auto load = [&](int bb) {
+      const int Lb = a.seq_lens[bb];
+      const int np = Lb > 0 ? min((int)(((long long)Lb + kPage - 1) / kPage), a.max_blocks) : 0;
+      return SeqLoad{(np + 1) / 2, Lb};
+    };
+    int pairs_b;
+    const SeqLoad first = map_first_loads(a, load);
+    if (!ragged_map(a, load, first, blockIdx.x, wi, pairs_b, L)) return;
+  } else {
+    wi.split = blockIdx.x;
+    wi.g = blockIdx.y;
+    wi.b = blockIdx.z;
+    wi.n_split = a.n_split;
+    wi.slot0 = (blockIdx.z * a.Hkv + blockIdx.y) * a.n_split;
+    L = a.seq_lens[wi.b];
+  }
+  const int split = wi.split, g = wi.g, b = wi.b, n_split = wi.n_split;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   const int n = lane & 15, j = lane >> 4;
   const int R = a.q_len * 4;
 
-  const int L = a.seq_lens[b];
   int np_seq = L > 0 ? (int)(((long long)L + kPage - 1) / kPage) : 0;
   np_seq = min(np_seq, a.max_blocks);
   // split `split` of n_split takes an even share of this sequence's page pairs;
   // its four wavefronts take those pairs round-robin
   const int pairs = (np_seq + 1) / 2;
-  const int q0 = (int)(((long long)split * pairs) / a.n_split);
-  const int q1 = (int)(((long long)(split + 1) * pairs) / a.n_split);
+  const int q0 = (int)(((long long)split * pairs) / n_split);
+  const int q1 = (int)(((long long)(split + 1) * pairs) / n_split);
   const int32_t *fbt = a.block_table + (size_t)b * a.bt_stride;
 
   // Q^T operand: row n of each tile, dims 32kb + 8j .. +7
@@ -378,28 +394,30 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
         if (r < R) {
           const size_t row = out_row(a, b, g, r);
           const float4 v = *reinterpret_cast<const float4 *>(&s_out[rr][d4]);
-          if (a.n_split == 1)
+          if (n_split == 1)
             *reinterpret_cast<float4 *>(a.out + row * kD + d4) = v;
           else
-            partial_store4(ro, ((row * a.n_split + split) * kD + d4) * 4, v);
+            partial_store4(ro, (((size_t)(wi.slot0 + split) * R + r) * kD + d4) * 4, v);
         }
       }
       if (threadIdx.x < 16 && nt * 16 + threadIdx.x < R) {
         const size_t row = out_row(a, b, g, nt * 16 + threadIdx.x);
-        if (a.n_split == 1) a.lse[row] = s_olse[threadIdx.x] * kLn2;
-        else partial_store1(rl, (row * a.n_split + split) * 4, s_olse[threadIdx.x]);
+        if (n_split == 1) a.lse[row] = s_olse[threadIdx.x] * kLn2;
+        else partial_store1(rl, ((size_t)(wi.slot0 + split) * R + nt * 16 + threadIdx.x) * 4,
+                            s_olse[threadIdx.x]);
       }
     }
     __syncthreads();
   }
 
   // ---- the last workgroup of (b, g) merges the splits ---------------------------------
-  if (a.n_split > 1 && last_arrival(a, b, g, &s_flag)) merge_rows(a, b, g, R);
+  if (n_split > 1 && last_arrival(a, b, g, n_split, &s_flag))
+    merge_rows(a, b, g, R, wi.slot0, n_split);
 }
 
 template <int KV>
 hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_split, a.Hkv, a.batch);
+  const dim3 grid = a.ragged ? dim3(a.n_split) : dim3(a.n_split, a.Hkv, a.batch);
   const int nt = (a.q_len * 4 + 15) / 16;
   switch (nt) {
     case 1: hipLaunchKernelGGL((verify_mfma_kernel<KV, 1>), grid, dim3(256), 0, s, a); break;

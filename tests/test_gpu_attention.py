@@ -168,6 +168,16 @@ def test_config5_fp8_verify_each_window_size():
     verify_check(w, pool, sorted(first.values()), batches=[0, 17, 63], kv_heads=[0, 5])
 
 
+def test_balanced_map_beyond_64_sequences():
+    # 100 ragged fp8 sequences of 4K-16K tokens (800 (sequence, KV head) units:
+    # the balanced split map, which takes two passes over the batch); the
+    # oracle checks sequences 0, 63, 64, 65, 99 (decode) and 0, 64, 99 x KV
+    # heads 0, 7 (verify)
+    w, pool = workload(5, batch=100, seq_len=16384)
+    decode_check(w, pool, [0], batches=[0, 63, 64, 65, 99])
+    verify_check(w, pool, [0], batches=[0, 64, 99], kv_heads=[0, 7])
+
+
 # --------------------------------------------------------------------------
 # cross-checks and edge cases on small shapes (several tiles + ragged tails)
 # --------------------------------------------------------------------------
