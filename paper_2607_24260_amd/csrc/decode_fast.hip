@@ -76,15 +76,10 @@ __device__ __forceinline__ float xor32_sum(float x) {
   return __int_as_float(r[0]) + __int_as_float(r[1]);
 }
 
-// pack the upper halves of two floats (exact bf16 values) into bf16x2
-__device__ __forceinline__ uint32_t pack_bf16_exact(float lo, float hi) {
-  return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
-}
-
 // Raw registers of one page: K slice and V^T slice of this lane.
 template <int KV> struct PageRegs;
 template <> struct PageRegs<kBF16> { u32x4 k[4]; u32x4 v[4]; };
-template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x2 v[4]; };
+template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x2 v[4]; float2 sc; };   // sc: (K, V) scales
 
 // Loads of one (page, head) tile. With live == false the descriptor covers
 // zero bytes: the loads return zeros without touching memory (used for
@@ -109,6 +104,7 @@ __device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, in
     for (int i = 0; i < 4; ++i) r.k[i] = tile_load8(kr, i * 512 + c * 128 + t * 8);
 #pragma unroll
     for (int i = 0; i < 4; ++i) r.v[i] = tile_load8(vr, i * 512 + lane * 8);
+    r.sc = page_scales(a.kv_scales, page, live);
   }
 }
 
@@ -123,10 +119,9 @@ __device__ __forceinline__ void k_pairs(const PageRegs<KV> &r, uint32_t kk[4][4]
     } else {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const float2 f0 = fp8x2_to_f32<false>(r.k[i][h]);
-        const float2 f1 = fp8x2_to_f32<true>(r.k[i][h]);
-        kk[i][2 * h] = pack_bf16_exact(f0.x, f0.y);
-        kk[i][2 * h + 1] = pack_bf16_exact(f1.x, f1.y);
+        const kv_u32x2 w = fp8x4_to_bf16x4(r.k[i][h]);
+        kk[i][2 * h] = w[0];
+        kk[i][2 * h + 1] = w[1];
       }
     }
   }
@@ -283,8 +278,8 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   auto process = [&](const PageRegs<KV> &cur, int page, int nvalid) {
     float ksc = a.scale_log2, vsc = 1.f;
     if constexpr (KV == kFP8) {
-      ksc *= a.kv_scales[2 * (size_t)page];
-      vsc = a.kv_scales[2 * (size_t)page + 1];
+      ksc *= cur.sc.x;
+      vsc = cur.sc.y;
     }
     // ---- logits --------------------------------------------------------------
     uint32_t kk[4][4];
@@ -316,7 +311,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     pm = xor32_max(pm);
     const float m_new = fmaxf(m_c, pm);
     if (__any(m_new > m_c)) {
-      const float alpha = exp2f(m_c - (m_new == -INFINITY ? 0.f : m_new));
+      const float alpha = exp2_fast(m_c - (m_new == -INFINITY ? 0.f : m_new));
       l_c *= alpha;
       float al[4];
 #pragma unroll
@@ -328,7 +323,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
         for (int i = 0; i < 4; ++i) acc[hh][i] *= al[hh];
       m_c = m_new;
     }
-    const float p = exp2f(s - (m_c == -INFINITY ? 0.f : m_c));
+    const float p = exp2_fast(s - (m_c == -INFINITY ? 0.f : m_c));
     l_c += p;
     pbuf[wave][lane] = p * vsc;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

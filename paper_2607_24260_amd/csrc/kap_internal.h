@@ -128,6 +128,15 @@ __device__ __forceinline__ uint32_t tile_load4(__amdgpu_buffer_rsrc_t r, int off
   return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kNonTemporal);
 }
 
+// The (K, V) fp8 scales of a page, loaded with the page's KV data (in the
+// same in-order vector-memory stream, so they arrive with it); a dead page
+// reads nothing and gets (0, 0). Every KV head reads them, so they are
+// cached normally.
+__device__ __forceinline__ float2 page_scales(const float *kv_scales, int page, bool live) {
+  const auto r = tile_rsrc(kv_scales, (size_t)page * 8, live ? 8 : 0);
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, 0, 0, 0));
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -144,6 +153,20 @@ __device__ __forceinline__ float2 fp8x2_to_f32(uint32_t w) {
   auto v = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w), HIGH);
   return make_float2(v[0], v[1]);
 }
+
+// Four E4M3FN codes (one dword) -> two dwords of bf16 pairs, exact (every
+// E4M3FN value, subnormals included, is a bf16 value); unit scale.
+typedef __bf16 kv_bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ kv_u32x2 fp8x4_to_bf16x4(uint32_t w) {
+  const kv_bf16x2 lo = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false);
+  const kv_bf16x2 hi = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true);
+  return kv_u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+}
+
+// 2^x on the hardware unit, without the range reduction that keeps
+// denormal results: results below 2^-126 may come out as 0. Used for softmax
+// weights, whose sum is at least 1.
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // One E4M3FN code -> float (generic path).
 __device__ __forceinline__ float fp8_to_f32(uint8_t b) {

@@ -20,8 +20,9 @@
 //                                               holds lane for lane.
 // Lane (j = lane/16, n = lane%16) thus owns query row n of each 16-row tile and
 // keys 4j..4j+3 of both pages, so the online softmax needs only two cross-row
-// steps per page pair. P is split into bf16 hi + lo parts (two PV products),
-// which keeps the probability rounding error below 2^-16 relative.
+// steps per page pair. P is split into bf16 hi + lo parts (two PV products):
+// hi = P truncated to bf16, lo = P - hi (exact in fp32) truncated to bf16,
+// which keeps the probability rounding error below 2^-14 relative.
 // The causal mask and the partial last page are handled on the last pages only.
 // The four wavefronts combine through LDS; with several splits, the workgroup
 // that finishes last for its (sequence, KV head) merges all splits (atomic
@@ -64,46 +65,51 @@ __device__ __forceinline__ uint32_t pack_bf16_exact(float lo, float hi) {
   return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
 }
 
-// 4 E4M3FN codes (one dword) -> 2 dwords of bf16 pairs, exact
-__device__ __forceinline__ u32x2 fp8x4_to_bf16x4(uint32_t w) {
-  const float2 f0 = fp8x2_to_f32<false>(w);
-  const float2 f1 = fp8x2_to_f32<true>(w);
-  return u32x2{pack_bf16_exact(f0.x, f0.y), pack_bf16_exact(f1.x, f1.y)};
-}
-
 constexpr int kTileBytes(int kv) { return (kv == kBF16 ? 2 : 1) * kPage * kD; }
 
-// K tile operand of one page for k-block kb: key n, dims 32kb + 8j .. +7
-// (chunk 4kb + j of the page's chunk-major K tile)
+// Raw registers of one page pair (pages k, k+1 of the sequence) as loaded:
+// bf16 operands, or fp8 codes that are widened only where they are used (a
+// conversion next to the load would make the load wait at once).
+template <int KV> struct PairData;
+template <> struct PairData<kBF16> {
+  u32x4 kA[4], kB[4];   // K operand: key n, dims 32kb + 8j .. +7 (8 bf16)
+  u32x2 vA[8], vB[8];   // V^T operand half: dim 16dt + n, keys 4j .. 4j+3 (4 bf16)
+};
+template <> struct PairData<kFP8> {
+  u32x2 kA[4], kB[4];   // the same elements as fp8 codes
+  uint32_t vA[8], vB[8];
+  float2 scA, scB;      // (K, V) scales of the two pages
+};
 template <int KV>
-__device__ __forceinline__ u32x4 load_k(__amdgpu_buffer_rsrc_t r, int n, int j, int kb) {
-  if constexpr (KV == kBF16) {
-    return tile_load16(r, kb * 1024 + j * 256 + n * 16);
-  } else {
-    const u32x2 w = tile_load8(r, kb * 512 + j * 128 + n * 8);
-    const u32x2 lo = fp8x4_to_bf16x4(w[0]), hi = fp8x4_to_bf16x4(w[1]);
-    return u32x4{lo[0], lo[1], hi[0], hi[1]};
-  }
-}
-
-// V^T operand half: dim dt*16 + n, keys 4j .. 4j+3 of one page, as 2 dwords of bf16
-template <int KV>
-__device__ __forceinline__ u32x2 load_vt(__amdgpu_buffer_rsrc_t r, int n, int j, int dt) {
-  if constexpr (KV == kBF16) {
-    return tile_load8(r, dt * 512 + n * 32 + j * 8);
-  } else {
-    return fp8x4_to_bf16x4(tile_load4(r, dt * 256 + n * 16 + j * 4));
-  }
-}
-
-// Loaded operands of one page pair (pages k, k+1 of the sequence).
-template <int KV>
-struct PairRegs {
-  u32x4 kA[4], kB[4];
-  u32x2 vA[8], vB[8];
+struct PairRegs : PairData<KV> {
   int pA, pB;
   bool okA, okB;
 };
+
+// K tile operand of one page for k-block kb: key n, dims 32kb + 8j .. +7
+// (chunk 4kb + j of the page's chunk-major K tile)
+__device__ __forceinline__ u32x4 load_k(__amdgpu_buffer_rsrc_t r, int n, int j, int kb, u32x4) {
+  return tile_load16(r, kb * 1024 + j * 256 + n * 16);
+}
+__device__ __forceinline__ u32x2 load_k(__amdgpu_buffer_rsrc_t r, int n, int j, int kb, u32x2) {
+  return tile_load8(r, kb * 512 + j * 128 + n * 8);
+}
+// V^T operand half: dim dt*16 + n, keys 4j .. 4j+3 of one page
+__device__ __forceinline__ u32x2 load_vt(__amdgpu_buffer_rsrc_t r, int n, int j, int dt, u32x2) {
+  return tile_load8(r, dt * 512 + n * 32 + j * 8);
+}
+__device__ __forceinline__ uint32_t load_vt(__amdgpu_buffer_rsrc_t r, int n, int j, int dt,
+                                            uint32_t) {
+  return tile_load4(r, dt * 256 + n * 16 + j * 4);
+}
+// ... and as bf16 operands
+__device__ __forceinline__ u32x4 k_operand(u32x4 x) { return x; }
+__device__ __forceinline__ u32x4 k_operand(u32x2 x) {
+  const u32x2 lo = fp8x4_to_bf16x4(x[0]), hi = fp8x4_to_bf16x4(x[1]);
+  return u32x4{lo[0], lo[1], hi[0], hi[1]};
+}
+__device__ __forceinline__ u32x2 v_operand(u32x2 x) { return x; }
+__device__ __forceinline__ u32x2 v_operand(uint32_t x) { return fp8x4_to_bf16x4(x); }
 
 // Pair at pages k, k+1 (k + 1 may lie past the sequence). Missing or invalid
 // pages, and pairs past the wavefront's share (live == false), load through a
@@ -125,13 +131,17 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, co
   const auto vrb = tile_rsrc(a.v_pages, ((size_t)r.pB * a.Hkv + g) * tile, bb);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
-    r.kA[kb] = load_k<KV>(kra, n, j, kb);
-    r.kB[kb] = load_k<KV>(krb, n, j, kb);
+    r.kA[kb] = load_k(kra, n, j, kb, r.kA[kb]);
+    r.kB[kb] = load_k(krb, n, j, kb, r.kB[kb]);
   }
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) {
-    r.vA[dt] = load_vt<KV>(vra, n, j, dt);
-    r.vB[dt] = load_vt<KV>(vrb, n, j, dt);
+    r.vA[dt] = load_vt(vra, n, j, dt, r.vA[dt]);
+    r.vB[dt] = load_vt(vrb, n, j, dt, r.vB[dt]);
+  }
+  if constexpr (KV == kFP8) {
+    r.scA = page_scales(a.kv_scales, r.pA, r.okA);
+    r.scB = page_scales(a.kv_scales, r.pB, r.okB);
   }
 }
 
@@ -216,14 +226,16 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
 
     float kscA = a.scale_log2, kscB = a.scale_log2, vscA = 1.f, vscB = 1.f;
     if constexpr (KV == kFP8) {
-      if (P.okA) {
-        kscA *= a.kv_scales[2 * (size_t)P.pA];
-        vscA = a.kv_scales[2 * (size_t)P.pA + 1];
-      }
-      if (P.okB) {
-        kscB *= a.kv_scales[2 * (size_t)P.pB];
-        vscB = a.kv_scales[2 * (size_t)P.pB + 1];
-      }
+      kscA *= P.scA.x;
+      vscA = P.scA.y;
+      kscB *= P.scB.x;
+      vscB = P.scB.y;
+    }
+    u32x2 vA[8], vB[8];   // V^T operand halves as bf16
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      vA[dt] = v_operand(P.vA[dt]);
+      vB[dt] = v_operand(P.vB[dt]);
     }
 
     // keys at or beyond L hold no data: zero their V so 0 * garbage cannot occur
@@ -235,10 +247,17 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
         const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          if (zA) P.vA[dt][e >> 1] &= mask;
-          if (zB) P.vB[dt][e >> 1] &= mask;
+          if (zA) vA[dt][e >> 1] &= mask;
+          if (zB) vB[dt][e >> 1] &= mask;
         }
       }
+    }
+
+    u32x4 kA[4], kB[4];   // K operands as bf16
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      kA[kb] = k_operand(P.kA[kb]);
+      kB[kb] = k_operand(P.kB[kb]);
     }
 
     // ---- S^T = K Q^T ------------------------------------------------------------
@@ -249,8 +268,8 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
       sB[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
-        sA[nt] = mfma(P.kA[kb], qop[nt][kb], sA[nt]);
-        sB[nt] = mfma(P.kB[kb], qop[nt][kb], sB[nt]);
+        sA[nt] = mfma(kA[kb], qop[nt][kb], sA[nt]);
+        sB[nt] = mfma(kB[kb], qop[nt][kb], sB[nt]);
       }
     }
 
@@ -281,34 +300,33 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
       const float m_new = fmaxf(m[nt], mx);
       const float mref = (m_new == -INFINITY) ? 0.f : m_new;
       if (m_new > m[nt]) {
-        const float alpha = exp2f(m[nt] - mref);
+        const float alpha = exp2_fast(m[nt] - mref);
         l[nt] *= alpha;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) acc[nt][dt] *= alpha;
         m[nt] = m_new;
       }
       float ps = 0.f;
-      uint32_t hb[8], lb[8];
+      float pv[8], pl[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = exp2f(z[e] - mref);
+        const float p = exp2_fast(z[e] - mref);
         ps += p;
-        const float pv = p * (e < 4 ? vscA : vscB);
-        const uint32_t hbits = f32_to_bf16_rne(pv);
-        hb[e] = hbits;
-        lb[e] = f32_to_bf16_rne(pv - __uint_as_float(hbits << 16));
+        pv[e] = p * (e < 4 ? vscA : vscB);
+        pl[e] = pv[e] - __uint_as_float(__float_as_uint(pv[e]) & 0xffff0000u);
       }
       l[nt] += ps;
-      phi[nt] = u32x4{hb[0] | (hb[1] << 16), hb[2] | (hb[3] << 16), hb[4] | (hb[5] << 16),
-                      hb[6] | (hb[7] << 16)};
-      plo[nt] = u32x4{lb[0] | (lb[1] << 16), lb[2] | (lb[3] << 16), lb[4] | (lb[5] << 16),
-                      lb[6] | (lb[7] << 16)};
+      // bf16 pairs are the upper halves of the floats (truncation)
+      phi[nt] = u32x4{pack_bf16_exact(pv[0], pv[1]), pack_bf16_exact(pv[2], pv[3]),
+                      pack_bf16_exact(pv[4], pv[5]), pack_bf16_exact(pv[6], pv[7])};
+      plo[nt] = u32x4{pack_bf16_exact(pl[0], pl[1]), pack_bf16_exact(pl[2], pl[3]),
+                      pack_bf16_exact(pl[4], pl[5]), pack_bf16_exact(pl[6], pl[7])};
     }
 
     // ---- O^T += V^T P^T -----------------------------------------------------------
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const u32x4 vop = u32x4{P.vA[dt][0], P.vA[dt][1], P.vB[dt][0], P.vB[dt][1]};
+      const u32x4 vop = u32x4{vA[dt][0], vA[dt][1], vB[dt][0], vB[dt][1]};
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         acc[nt][dt] = mfma(vop, phi[nt], acc[nt][dt]);
