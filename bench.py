@@ -436,6 +436,51 @@ def main():
         f"cache-hot {t_dec_hot * 1e3:.2f} us; verify: {t_ver * 1e3:.1f} us/call "
         f"({ver_gbs:.0f} GB/s); plan: {t_plan * 1e3:.1f} us")
 
+    # compaction into a compact workspace (the paper's materialised view) against
+    # the zero-copy view, and the slot-mapped append of one verify window
+    maint = None
+    if cfg == 4:
+        cap_c = 512
+        kv0 = kvs[0]
+        comp = [K.KVCache(torch.empty((B * cap_c,) + tuple(kv0.k_pages.shape[1:]),
+                                      dtype=kv0.k_pages.dtype, device=dev),
+                          torch.empty((B * cap_c,) + tuple(kv0.v_pages.shape[1:]),
+                                      dtype=kv0.v_pages.dtype, device=dev), Hq, qdt)
+                for _ in range(R)]
+        ctab = torch.empty((B, cap_c), dtype=torch.int32, device=dev)
+        vbt_, vnb_ = plan_out["view_block_table"], plan_out["view_num_blocks"]
+        t_comp = time_loop(lambda i: K.compact_view(kvs[i % R], vbt_, vnb_, cap_c, comp[i % R],
+                                                    out=ctab), 45, 3, torch)
+        lblk_c = plan_out["view_logical_block"][:, :cap_c].contiguous()
+        o_c = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        l_c = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        ws_c = torch.zeros(max(256, K.selected_decode_workspace_bytes(comp[0], B, cap_c)),
+                           dtype=torch.uint8, device=dev)
+        dec_c = [K.bind_selected_decode(comp[c], w.q_decode[0], seq_lens, ctab, lblk_c,
+                                        plan_out["view_num_blocks"], cap_c, w.sm_scale, o_c, l_c,
+                                        ws_c) for c in range(R)]
+        t_dec_c = time_loop(lambda i: dec_c[i % R](), 256, 5, torch)
+        win = q_len * B
+        Lh = np.asarray(w.seq_lens, dtype=np.int64)
+        fbh = np.asarray(w.full_block_table, dtype=np.int64)
+        pos = [Lh[b] - q_len + np.arange(q_len) for b in range(B)]
+        slots = torch.as_tensor(np.concatenate([fbh[b, p // 16] * 16 + p % 16
+                                                for b, p in enumerate(pos)])).to(dev)
+        k_win = torch.randn((win, w.num_kv_heads, D), device=dev).to(kv0.k_pages.dtype)
+        v_win = torch.randn((win, w.num_kv_heads, D), device=dev).to(kv0.k_pages.dtype)
+        t_app = time_loop(lambda i: K.append_kv(kvs[i % R], k_win, v_win, slots), 200, 3, torch)
+        comp_bytes = 2 * (int(np.sum(view_blocks)) * 16 * BYTES_PER_TOKEN[w.kv_dtype])
+        maint = {
+            "compact_view_us": round(t_comp * 1e3, 2),
+            "compact_view_gbs": round(comp_bytes / (t_comp * 1e-3) / 1e9, 1),
+            "compact_view_bytes": comp_bytes,
+            "decode_on_compact_us": round(t_dec_c * 1e3, 2),
+            "zero_copy_decode_us": round(t_dec * 1e3, 2),
+            "append_window_us": round(t_app * 1e3, 2),
+            "append_window_tokens": win,
+        }
+        log(f"kv maintenance: {maint}")
+
     ragged = None
     if not args.no_ragged and cfg == 4:
         ragged = ragged_stream(torch, K, dev)
@@ -491,6 +536,7 @@ def main():
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
             "traffic": counter_traffic("decode_fast_kernel") if cfg == 4 else None,
         },
+        "kv_maintenance": maint,
         "ragged_fp8_stream": ragged,
         "cpu_baseline": cpu,
     }

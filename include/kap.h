@@ -219,6 +219,50 @@ kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, cons
 size_t kap_verify_workspace_bytes(const kap_kv_cache *kv, int32_t batch, int32_t q_len,
                                   int32_t max_seq_len, int32_t num_splits);
 
+/*
+ * kap_append_kv -- place newly scheduled tokens' K/V into their physical KV
+ * slots (the slot mapping of Sec. 3.1, "Selected-KV view materialization"):
+ * how verification advances the full-context KV state KV^{full,+} of Sec. 3.2
+ * ("Full-context verification").
+ *
+ * Token t goes to slot slot_mapping[t] = page * 16 + offset of the pool
+ * described by kv, whose k_pages / v_pages this call WRITES (the const of the
+ * struct fields notwithstanding). k_new / v_new [num_tokens][Hkv][D] hold the
+ * values as the pool stores them (kv_dtype: f32, bf16 bits, or E4M3FN codes
+ * already quantised with the destination page's scale -- kv_scales are not
+ * changed); they are copied bit for bit into the page layout (K in 8-dim
+ * chunks, V dim-major). A negative slot is padding and is skipped; a slot at
+ * or beyond num_pages * 16 is skipped and counted into *bad_slots (device
+ * int32, may be NULL; the caller zeroes it). Two tokens with the same slot:
+ * either may win. num_tokens = 0 is a no-op.
+ */
+kap_status kap_append_kv(const kap_kv_cache *kv, int32_t num_tokens, const void *k_new,
+                         const void *v_new, const int64_t *slot_mapping, int32_t *bad_slots,
+                         void *stream);
+
+/*
+ * kap_compact_view -- materialise the selected-KV view as a compact physical
+ * copy (Alg. 1, AssignCompactSlots and BuildBlockTable; Sec. 3.1: the
+ * selected pages are compacted in access order into a reusable compact
+ * workspace whose capacity is fixed).
+ *
+ * For sequence b and k < min(view_num_blocks[b], view_capacity), page
+ * view_block_table[b][k] of src (K, V and, for fp8, its two scales) is copied
+ * to page b * view_capacity + k of dst, and compact_block_table[b][k] is set
+ * to that page; entries k >= the view length are set to -1. Invalid source
+ * page ids copy nothing and map to -1. dst must have the same geometry and
+ * dtypes as src and at least batch * view_capacity pages. Decoding over
+ * (dst, compact_block_table, the same view_logical_block and view_num_blocks)
+ * gives the result of decoding over (src, view_block_table).
+ *   view_block_table [batch][view_stride], compact_block_table
+ *   [batch][view_capacity] int32; view_capacity <= view_stride.
+ */
+kap_status kap_compact_view(const kap_kv_cache *src, int32_t batch,
+                            const int32_t *view_block_table, int32_t view_stride,
+                            const int32_t *view_num_blocks, int32_t view_capacity,
+                            const kap_kv_cache *dst, int32_t *compact_block_table,
+                            void *stream);
+
 /* Static description of a status code. */
 const char *kap_status_string(kap_status status);
 /* Message of the last failing call on this thread ("" if none). */

@@ -16,6 +16,10 @@ Systems" (arXiv 2607.24260). What is computed, and where it is defined:
   step attends only to the prompt-side KV pages the plan exposes.
 * ``verify`` -- Sec. 3.2, "Full-context verification" and Eq. (2): a window of
   k+1 query tokens attends causally to the full KV cache.
+* ``append_kv`` / ``compact_view`` -- Sec. 3.1 slot mappings and compact
+  workspace (Alg. 1, AssignCompactSlots / BuildBlockTable): placing new
+  tokens into their KV slots, and copying a view's pages into a compact
+  workspace of fixed capacity.
 * ``lse_merge`` -- the exact softmax identity used to combine attention over
   disjoint key sets (a standard identity, not stated in the paper).
 * ``e4m3fn_to_f64`` / ``bf16_to_f64`` -- decoding of stored KV bits (OCP 8-bit
@@ -283,10 +287,17 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_visible: Sequence[int]
     return o, lse
 
 
-def _view_tokens(pool: KVPool, g: int, seq_len: int, pages, lblks):
-    """K and V of the visible tokens of a list of (physical, logical) pages."""
+def _view_tokens(pool: KVPool, g: int, seq_len: int, pages, lblks, skip_invalid: bool = True):
+    """K and V of the visible tokens of a list of (physical, logical) pages.
+
+    A view entry whose page id lies outside the pool contributes no keys (the
+    reading the boundary documents for ids kap_compile_plan would report as
+    KAP_PLAN_BAD_PAGE)."""
     pages = np.asarray(pages, dtype=np.int64)
     lblks = np.asarray(lblks, dtype=np.int64)
+    if skip_invalid:
+        ok = (pages >= 0) & (pages < pool.k_pages.shape[0])
+        pages, lblks = pages[ok], lblks[ok]
     if len(pages) == 0:
         D = pool.v_pages.shape[2]
         return np.zeros((0, D)), np.zeros((0, D))
@@ -330,7 +341,7 @@ def full_tokens(pool: KVPool, g: int, seq_len: int, fbt_row):
     """K and V of all tokens 0 .. seq_len-1 of one sequence, in logical order."""
     npages = -(-int(seq_len) // PAGE)
     pages = np.asarray(fbt_row)[:npages]
-    return _view_tokens(pool, g, int(seq_len), pages, np.arange(npages))
+    return _view_tokens(pool, g, int(seq_len), pages, np.arange(npages), skip_invalid=False)
 
 
 def verify(pool: KVPool, q: np.ndarray, seq_lens, full_block_table,
@@ -403,3 +414,69 @@ def split_attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, bounds: Sequence[i
         parts_o.append(ob)
         parts_l.append(lb)
     return lse_merge(np.stack(parts_o), np.stack(parts_l))
+
+
+# --------------------------------------------------------------------------
+# KV maintenance: slot-mapped append and view compaction
+# --------------------------------------------------------------------------
+
+def append_kv(pool: KVPool, k_new: np.ndarray, v_new: np.ndarray, slot_mapping):
+    """Place new tokens' stored K/V values into their physical slots.
+
+    Sec. 3.1 ("Selected-KV view materialization"): slot mappings place newly
+    scheduled tokens into their KV slots; Sec. 3.2 ("Full-context
+    verification"): this is how the full-context state KV^{full,+} advances.
+
+    k_new / v_new: [T][Hkv][D] in the pool's storage dtype. Token t goes to
+    slot s = slot_mapping[t] = page * PAGE + offset: dim d of KV head g is
+    element [page][g][d // 8][offset][d % 8] of k_pages and [page][g][d][offset]
+    of v_pages. Negative slots are skipped; slots past the pool are skipped
+    and counted. Returns (new pool, number of out-of-range slots).
+    """
+    k = np.array(pool.k_pages, copy=True)
+    v = np.array(pool.v_pages, copy=True)
+    P, Hkv, C, _, E = k.shape
+    bad = 0
+    for t, s in enumerate(np.asarray(slot_mapping, dtype=np.int64)):
+        s = int(s)
+        if s < 0:
+            continue
+        if s >= P * PAGE:
+            bad += 1
+            continue
+        page, off = divmod(s, PAGE)
+        k[page, :, :, off, :] = np.asarray(k_new[t]).reshape(Hkv, C, E)
+        v[page, :, :, off] = np.asarray(v_new[t])
+    return KVPool(k, v, pool.dtype, pool.scales), bad
+
+
+def compact_view(pool: KVPool, view_block_table, view_num_blocks, capacity: int):
+    """Copy each sequence's selected pages into a compact workspace.
+
+    Alg. 1, AssignCompactSlots and BuildBlockTable; Sec. 3.1: the selected
+    pages are compacted in access order into a workspace of fixed capacity.
+    View entry k < min(view_num_blocks[b], capacity) of sequence b (a valid
+    page id) goes to compact page b * capacity + k (K, V and fp8 scales);
+    the compact block table holds that page, or -1. Compact pages that receive
+    nothing are left zero. Returns (compact pool, table [B][capacity]).
+    """
+    vbt = np.asarray(view_block_table, dtype=np.int64)
+    nb = np.asarray(view_num_blocks, dtype=np.int64)
+    B = len(nb)
+    P = pool.k_pages.shape[0]
+    k = np.zeros((B * capacity,) + pool.k_pages.shape[1:], dtype=pool.k_pages.dtype)
+    v = np.zeros((B * capacity,) + pool.v_pages.shape[1:], dtype=pool.v_pages.dtype)
+    sc = None if pool.scales is None else np.zeros((B * capacity, 2), dtype=np.float32)
+    table = np.full((B, capacity), -1, dtype=np.int64)
+    for b in range(B):
+        for j in range(min(int(nb[b]), capacity)):
+            p = int(vbt[b, j])
+            if not 0 <= p < P:
+                continue
+            dst = b * capacity + j
+            k[dst] = pool.k_pages[p]
+            v[dst] = pool.v_pages[p]
+            if sc is not None:
+                sc[dst] = pool.scales[p]
+            table[b, j] = dst
+    return KVPool(k, v, pool.dtype, sc), table

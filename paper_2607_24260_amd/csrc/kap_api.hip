@@ -499,4 +499,95 @@ kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, cons
   return launch_attention(a, kv, p, false, workspace, static_cast<hipStream_t>(stream));
 }
 
+// ---------------------------------------------------------------------------
+// kap_append_kv / kap_compact_view
+// ---------------------------------------------------------------------------
+
+static int elem_bytes(kap_dtype t) {
+  return t == KAP_DT_F32 ? 4 : (t == KAP_DT_BF16 ? 2 : 1);
+}
+
+kap_status kap_append_kv(const kap_kv_cache *kv, int32_t num_tokens, const void *k_new,
+                         const void *v_new, const int64_t *slot_mapping, int32_t *bad_slots,
+                         void *stream) {
+  kap_status st = check_kv(kv);
+  if (st != KAP_OK) return st;
+  if (num_tokens < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_tokens < 0");
+  if (num_tokens == 0) return ok();
+  if (num_tokens > 0x7fffffff / 2) return fail(KAP_ERR_UNSUPPORTED, "too many tokens");
+  if (!k_new || !v_new || !slot_mapping)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "k_new, v_new and slot_mapping are required");
+  if (kv->num_pages < 1) return fail(KAP_ERR_INVALID_ARGUMENT, "KV pool has no pages");
+  kap::AppendArgs a;
+  a.num_tokens = num_tokens;
+  a.Hkv = kv->num_kv_heads;
+  a.D = kv->head_dim;
+  a.elem_bytes = elem_bytes(kv->kv_dtype);
+  if (!aligned(k_new, a.elem_bytes) || !aligned(v_new, a.elem_bytes) || !aligned(slot_mapping, 8))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "k_new / v_new / slot_mapping misaligned");
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.slots = slot_mapping;
+  a.k_pages = const_cast<void *>(kv->k_pages);
+  a.v_pages = const_cast<void *>(kv->v_pages);
+  a.num_pages = kv->num_pages;
+  a.bad_slots = bad_slots;
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_append_kv(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+kap_status kap_compact_view(const kap_kv_cache *src, int32_t batch,
+                            const int32_t *view_block_table, int32_t view_stride,
+                            const int32_t *view_num_blocks, int32_t view_capacity,
+                            const kap_kv_cache *dst, int32_t *compact_block_table,
+                            void *stream) {
+  kap_status st = check_kv(src);
+  if (st != KAP_OK) return st;
+  st = check_kv(dst);
+  if (st != KAP_OK) return st;
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (view_capacity < 0 || view_stride < view_capacity)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "need 0 <= view_capacity (%d) <= view_stride (%d)",
+                view_capacity, view_stride);
+  if (batch == 0 || view_capacity == 0) return ok();
+  if (src->num_kv_heads != dst->num_kv_heads || src->num_q_heads != dst->num_q_heads ||
+      src->head_dim != dst->head_dim || src->kv_dtype != dst->kv_dtype ||
+      src->q_dtype != dst->q_dtype)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "src and dst caches differ in geometry or dtype");
+  const long long need = (long long)batch * view_capacity;
+  if (dst->num_pages < need)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "dst holds %lld pages, needs batch * view_capacity = %lld",
+                (long long)dst->num_pages, need);
+  if (need > 0x7fffffffLL) return fail(KAP_ERR_UNSUPPORTED, "compact workspace too large");
+  if (!view_block_table || !view_num_blocks || !compact_block_table)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (!aligned(dst->k_pages, 16) || !aligned(dst->v_pages, 16))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "dst pages must be 16-byte aligned");
+  kap::CompactArgs a;
+  a.batch = batch;
+  a.capacity = view_capacity;
+  a.view_stride = view_stride;
+  a.Hkv = src->num_kv_heads;
+  a.D = src->head_dim;
+  a.elem_bytes = elem_bytes(src->kv_dtype);
+  a.view_bt = view_block_table;
+  a.view_num_blocks = view_num_blocks;
+  a.src_k = src->k_pages;
+  a.src_v = src->v_pages;
+  a.src_scales = src->kv_dtype == KAP_DT_FP8_E4M3FN ? src->kv_scales : nullptr;
+  a.src_pages = src->num_pages;
+  a.dst_k = const_cast<void *>(dst->k_pages);
+  a.dst_v = const_cast<void *>(dst->v_pages);
+  a.dst_scales = const_cast<float *>(dst->kv_scales);
+  a.compact_bt = compact_block_table;
+  // enough workgroups to stream at full bandwidth; each strides over entries
+  const long long grid = need < 4LL * device_cus() ? need : 4LL * device_cus();
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_compact_view(a, (int)grid, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

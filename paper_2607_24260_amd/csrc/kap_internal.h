@@ -82,7 +82,31 @@ struct AttnArgs {
   float *lse;       // [batch * R]
 };
 
+// kap_append_kv after host validation.
+struct AppendArgs {
+  int num_tokens, Hkv, D, elem_bytes;
+  const void *k_new, *v_new;     // [num_tokens][Hkv][D]
+  const int64_t *slots;          // [num_tokens]
+  void *k_pages, *v_pages;       // the pool written into
+  int64_t num_pages;
+  int32_t *bad_slots;            // may be NULL
+};
+
+// kap_compact_view after host validation.
+struct CompactArgs {
+  int batch, capacity, view_stride, Hkv, D, elem_bytes;
+  const int32_t *view_bt, *view_num_blocks;
+  const void *src_k, *src_v;
+  const float *src_scales;       // fp8 only, else NULL
+  int64_t src_pages;
+  void *dst_k, *dst_v;
+  float *dst_scales;
+  int32_t *compact_bt;           // [batch][capacity]
+};
+
 hipError_t launch_compile_plan(const PlanArgs &a, hipStream_t s);
+hipError_t launch_append_kv(const AppendArgs &a, hipStream_t s);
+hipError_t launch_compact_view(const CompactArgs &a, int grid, hipStream_t s);
 hipError_t launch_attn_generic(const AttnArgs &a, hipStream_t s);
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s);
 hipError_t launch_verify_mfma(const AttnArgs &a, hipStream_t s);

@@ -146,6 +146,9 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, co
 }
 
 constexpr int kVerifyWaves = 4;
+// fp8 pairs in flight for windows of up to 8 tokens: two (fewer registers,
+// fewer spills; fp8 pairs are half the bytes of bf16 pairs)
+constexpr int kRingFP8Small = 2;
 
 template <int KV, int NT>
 __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
@@ -218,7 +221,7 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  // RING pair buffers (three; two for 9..12-token windows, one beyond),
+  // RING pair buffers (three, two for fp8; two for 9..12-token windows, one beyond),
   // unrolled: while one pair is processed the loads of the next ones are in
   // flight. Past the end of this wavefront's pairs the loads go through an
   // empty descriptor (no traffic), so the steady state is straight-line code.
@@ -343,7 +346,7 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
     // processing of pairs past the end: an early exit inside a round would
     // make the loop header wait for the just-issued loads, draining the ring
     // every round.
-    constexpr int RING = NT <= 2 ? 3 : (NT == 3 ? 2 : 1);
+    constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 ? 2 : 1);
     PairRegs<KV> rr[RING];
 #pragma unroll
     for (int jr = 0; jr < RING; ++jr)

@@ -44,6 +44,7 @@ EXPORTS = (
     "kap_compile_plan", "kap_compile_plan_workspace_bytes",
     "kap_selected_decode", "kap_selected_decode_workspace_bytes",
     "kap_verify", "kap_verify_workspace_bytes",
+    "kap_append_kv", "kap_compact_view",
     "kap_status_string", "kap_last_error", "kap_abi_version",
 )
 
@@ -106,6 +107,12 @@ def load_library(path: str = LIB_PATH):
     lib.kap_verify_workspace_bytes.restype = _SZ
     lib.kap_verify_workspace_bytes.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _I32, _I32, _I32]
+    lib.kap_append_kv.restype = _I32
+    lib.kap_append_kv.argtypes = [ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _P]
+    lib.kap_compact_view.restype = _I32
+    lib.kap_compact_view.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _P, _I32, _P, _I32, ctypes.POINTER(KVCacheStruct),
+        _P, _P]
     lib.kap_status_string.restype = ctypes.c_char_p
     lib.kap_status_string.argtypes = [_I32]
     lib.kap_last_error.restype = ctypes.c_char_p
@@ -209,6 +216,53 @@ class KVCache:
     @property
     def device(self):
         return self.k_pages.device
+
+
+# --------------------------------------------------------------------------
+# kap_append_kv / kap_compact_view
+# --------------------------------------------------------------------------
+
+def append_kv(kv: KVCache, k_new, v_new, slot_mapping, bad_slots=None, stream=None):
+    """Write new tokens' stored K/V ([T][Hkv][D], the pool's storage dtype)
+    into their slots (page * 16 + offset; negative = padding) of ``kv``, in
+    place. ``bad_slots`` (int32 [1], zeroed by the caller) counts slots past
+    the pool."""
+    lib = load_library()
+    T = int(slot_mapping.shape[0])
+    _dev(slot_mapping, "slot_mapping", torch.int64, 1)
+    shape = (T, kv.num_kv_heads, kv.head_dim)
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _dev(t, name, kv.k_pages.dtype)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} must be {shape}, got {tuple(t.shape)}")
+    if bad_slots is not None:
+        _dev(bad_slots, "bad_slots", torch.int32)
+    _check(lib.kap_append_kv(ctypes.byref(kv.struct), T, _ptr(k_new), _ptr(v_new),
+                             _ptr(slot_mapping), _ptr(bad_slots), _stream(stream)))
+
+
+def compact_view(src: KVCache, view_block_table, view_num_blocks, view_capacity: int,
+                 dst: KVCache, out=None, stream=None) -> torch.Tensor:
+    """Copy each sequence's first min(view_num_blocks[b], view_capacity) view
+    pages of ``src`` to pages b * view_capacity + k of ``dst``; returns the
+    compact block table [B][view_capacity] (int32, -1 where nothing was
+    copied)."""
+    lib = load_library()
+    _dev(view_block_table, "view_block_table", torch.int32, 2)
+    _dev(view_num_blocks, "view_num_blocks", torch.int32, 1)
+    B = int(view_num_blocks.shape[0])
+    if view_block_table.shape[0] != B:
+        raise ValueError("view_block_table and view_num_blocks disagree on the batch")
+    if out is None:
+        out = torch.empty((B, view_capacity), dtype=torch.int32, device=src.device)
+    _dev(out, "out", torch.int32, 2)
+    if tuple(out.shape) != (B, view_capacity):
+        raise ValueError(f"out must be {(B, view_capacity)}")
+    _check(lib.kap_compact_view(ctypes.byref(src.struct), B, _ptr(view_block_table),
+                                view_block_table.shape[1], _ptr(view_num_blocks),
+                                int(view_capacity), ctypes.byref(dst.struct), _ptr(out),
+                                _stream(stream)))
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -141,3 +141,28 @@ def test_binding_refuses_cpu_tensors():
     with pytest.raises(ValueError, match="GPU tensor"):
         K.KVCache(torch.zeros(2, 1, 16, 128, dtype=torch.bfloat16),
                   torch.zeros(2, 1, 128, 16, dtype=torch.bfloat16), 4, torch.bfloat16)
+
+
+def test_append_kv_rejects_bad_arguments(lib):
+    kv = kv_struct()
+    app = lambda n, k=FAKE, v=FAKE, s=FAKE: lib.kap_append_kv(ctypes.byref(kv), n, k, v, s, None, None)
+    assert app(-1) == K.KAP_ERR_INVALID_ARGUMENT
+    assert app(0) == K.KAP_OK                                     # no-op, nothing launched
+    assert app(4, k=None) == K.KAP_ERR_INVALID_ARGUMENT
+    assert app(4, s=FAKE + 4) == K.KAP_ERR_INVALID_ARGUMENT       # slot_mapping is int64
+    assert b"misaligned" in lib.kap_last_error()
+    bad = kv_struct(page=8)
+    assert lib.kap_append_kv(ctypes.byref(bad), 4, FAKE, FAKE, FAKE, None, None) \
+        == K.KAP_ERR_UNSUPPORTED
+
+
+def test_compact_view_rejects_bad_arguments(lib):
+    src = kv_struct(num_pages=100)
+    comp = lambda dst, batch=4, stride=16, cap=8, table=FAKE: lib.kap_compact_view(
+        ctypes.byref(src), batch, FAKE, stride, FAKE, cap, ctypes.byref(dst), table, None)
+    assert comp(kv_struct(num_pages=31)) == K.KAP_ERR_INVALID_ARGUMENT    # < batch * cap
+    assert b"needs batch * view_capacity" in lib.kap_last_error()
+    assert comp(kv_struct(num_pages=64), cap=17) == K.KAP_ERR_INVALID_ARGUMENT   # cap > stride
+    assert comp(kv_struct(num_pages=64, Hkv=4)) == K.KAP_ERR_INVALID_ARGUMENT    # geometry
+    assert comp(kv_struct(num_pages=64), table=None) == K.KAP_ERR_INVALID_ARGUMENT
+    assert comp(kv_struct(num_pages=0), batch=0) == K.KAP_OK                     # no-op
