@@ -166,12 +166,16 @@ def cpu_baseline(w, budget_s=12.0):
 
 def ragged_stream(torch, K, dev, reps=3):
     """The ragged fp8 workload (64 sequences of 4K..128K tokens, fp8 KV with
-    per-page scales, budgets 3%..30%) run as the executor runs it: one plan
-    compile, then 16 cycles of gamma in {2, 4, 8} proposal decode calls and one
-    verify window each, with seeded accept lengths and the h <= s fallback to
-    full-context access (the view arrays switch on the device). Timed with HIP
-    events over whole streams; rate = algorithmic bytes / time."""
-    from paper_2607_24260_amd.executor import FULL, FallbackPolicy, ViewBuilder, accepted_counts
+    per-page scales, budgets 3%..30%) run device-resident, as
+    executor.DeviceStream runs it: one plan compile, then 16 cycles of gamma in
+    {2, 4, 8} proposal decode calls and one verify window each, with seeded
+    accept lengths and the h <= s fallback to full-context access decided and
+    applied on the device (kap_fallback_update). Timed with HIP events over
+    whole streams, launched eagerly and as one HIP graph replay; rate =
+    algorithmic bytes / time (the bytes follow the host FallbackPolicy, which
+    makes the same decisions)."""
+    from paper_2607_24260_amd.executor import (FULL, DeviceStream, FallbackPolicy,
+                                               accepted_counts)
     from paper_2607_24260_amd.workloads import DESCRIPTIONS, make_workload
 
     w = make_workload(5, device=dev)
@@ -189,102 +193,94 @@ def ragged_stream(torch, K, dev, reps=3):
         "plan_status": torch.zeros(B, dtype=torch.int32, device=dev),
         "span_selected": torch.zeros(len(w.span_start), dtype=torch.int32, device=dev),
     }
+    ds_stream = torch.cuda.Stream(device=dev)
     ws_plan = torch.empty(max(K.compile_plan_workspace_bytes(B, len(w.span_start), w.fbt_stride),
                               256), dtype=torch.uint8, device=dev)
     plan_call = K.bind_compile_plan(seq_lens, fbt, i32(w.span_offsets), i32(w.span_start),
                                     i32(w.span_len), torch.as_tensor(w.span_prior).to(dev),
                                     i32(w.prefix), i32(w.suffix), i32(w.budget),
                                     num_pages=w.num_pages, view_capacity=cap, out=plan,
-                                    workspace=ws_plan)
-    torch.cuda.synchronize()
+                                    workspace=ws_plan, stream=ds_stream)
+    ds_stream.synchronize()
+    ds = DeviceStream(w, kv, plan, plan_call=plan_call, stream=ds_stream)
     status = plan["plan_status"].cpu().numpy()
     vtok = plan["view_tokens"].cpu().numpy().astype(np.int64)
     vblk = plan["view_num_blocks"].cpu().numpy().astype(np.int64)
     L = np.asarray(w.seq_lens, dtype=np.int64)
-    views = ViewBuilder(plan, fbt, w.seq_lens, cap)
-    o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
-    lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-    ws_dec = torch.zeros(max(256, K.selected_decode_workspace_bytes(kv, B, views.max_blocks)),
-                         dtype=torch.uint8, device=dev)
-    dec = [K.bind_selected_decode(kv, w.q_decode[i], seq_lens, views.vbt, views.vlb, views.vnb,
-                                  views.max_blocks, w.sm_scale, o, lse, ws_dec)
-           for i in range(w.q_decode.shape[0])]
-    ver, vbytes = [], []
-    for q in w.q_verify:
-        ql = q.shape[1]
-        ov = torch.empty((B, ql, Hq, D), dtype=torch.float32, device=dev)
-        lv = torch.empty((B, ql, Hq), dtype=torch.float32, device=dev)
-        wv = torch.zeros(max(256, K.verify_workspace_bytes(kv, B, ql, int(L.max()))),
-                         dtype=torch.uint8, device=dev)
-        ver.append(K.bind_verify(kv, q, seq_lens, fbt, int(L.max()), w.sm_scale, ov, lv, wv))
-        vbytes.append(algorithmic_bytes(w, None, None, "verify", ql))
-    gammas = [q.shape[1] - 1 for q in w.q_verify]
     pages_full = -(-L // 16)
+    gammas = [q.shape[1] - 1 for q in w.q_verify]
 
-    def decode_bytes(mode):
-        full = mode == FULL
-        tok = np.where(full, L, vtok)
-        pages = np.where(full, pages_full, vblk)
-        return int(tok.sum()) * 2048 + int(pages.sum()) * 16 + B * 8 + B * Hq * (D * 6 + 4)
+    # algorithmic bytes of one stream, following the (identical) host policy
+    policy = FallbackPolicy(vtok / L, status == K.KAP_PLAN_OK)
+    nbytes, n_dec, n_ver = plan_bytes(w, vblk), 0, 0
+    for kind, idx in w.schedule:
+        if kind == "decode":
+            full = policy.mode == FULL
+            tok = np.where(full, L, vtok)
+            pages = np.where(full, pages_full, vblk)
+            nbytes += int(tok.sum()) * 2048 + int(pages.sum()) * 16 + B * 8 + B * Hq * (D * 6 + 4)
+            n_dec += 1
+        else:
+            nbytes += algorithmic_bytes(w, None, None, "verify", gammas[idx] + 1)
+            policy.update(accepted_counts(w.accept_draws[idx], gammas[idx]), gammas[idx])
+            n_ver += 1
+    flips = int((policy.mode == FULL).sum())
 
-    def stream(events=None):
-        policy = FallbackPolicy(vtok / L, status == K.KAP_PLAN_OK)
-        views.apply(policy.mode)
-        plan_call()
-        nbytes, cycle, flips = 0, 0, 0
-        for kind, idx in w.schedule:
-            if kind == "decode":
-                dec[idx]()
-                nbytes += decode_bytes(policy.mode)
-                if events is not None:
-                    events.append(("decode", torch.cuda.Event(enable_timing=True)))
-                    events[-1][1].record()
-            else:
-                ver[idx]()
-                nbytes += vbytes[idx]
-                if events is not None:
-                    events.append(("verify", torch.cuda.Event(enable_timing=True)))
-                    events[-1][1].record()
-                f = policy.update(accepted_counts(w.accept_draws[cycle], gammas[idx]), gammas[idx])
-                if len(f):
-                    views.apply(policy.mode)
-                    flips += len(f)
-                cycle += 1
-        return nbytes, flips
+    def timed(launch, stream):
+        out = []
+        for _ in range(reps):
+            s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s_ev.record(stream)
+            launch()
+            e_ev.record(stream)
+            e_ev.synchronize()
+            out.append(s_ev.elapsed_time(e_ev))
+        return statistics.median(out)
 
-    stream()
+    ds.run()
+    ds_stream.synchronize()
+    ms_eager = timed(ds.run, ds_stream)
+    graph = ds.capture()
+    cur = torch.cuda.current_stream()
+    graph.replay()
     torch.cuda.synchronize()
-    times = []
-    for _ in range(reps):
-        s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s_ev.record()
-        nbytes, flips = stream()
-        e_ev.record()
-        e_ev.synchronize()
-        times.append(s_ev.elapsed_time(e_ev))
-    ms = statistics.median(times)
+    ms_graph = timed(graph.replay, cur)
+
+    # decode / verify split of one eager stream (events between the calls)
     ev = []
     t0 = torch.cuda.Event(enable_timing=True)
-    t0.record()
-    stream(ev)
-    torch.cuda.synchronize()
+    t0.record(ds_stream)
+    plan_call()
+    ds.reset()
+    for kind, idx in w.schedule:
+        if kind == "decode":
+            ds.decode[idx]()
+        else:
+            ds.verify[idx]()
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(ds_stream)
+        ev.append((kind, e))
+        if kind == "verify":
+            ds.update[idx]()
+    ds_stream.synchronize()
     dt = {"decode": 0.0, "verify": 0.0}
-    n = {"decode": 0, "verify": 0}
     prev = t0
     for kind, e in ev:
         dt[kind] += prev.elapsed_time(e)
-        n[kind] += 1
         prev = e
-    gbs = nbytes / (ms * 1e-3) / 1e9
+    gbs = nbytes / (ms_graph * 1e-3) / 1e9
     return {
         "workload": f"config5: {DESCRIPTIONS[5]}",
-        "ms_per_stream": round(ms, 3), "algorithmic_gb": round(nbytes / 1e9, 3),
+        "ms_per_stream_graph": round(ms_graph, 3), "ms_per_stream_eager": round(ms_eager, 3),
+        "algorithmic_gb": round(nbytes / 1e9, 3),
         "effective_gbs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
-        "decode_calls": n["decode"], "verify_calls": n["verify"],
-        "decode_us_mean": round(1e3 * dt["decode"] / max(n["decode"], 1), 2),
-        "verify_us_mean": round(1e3 * dt["verify"] / max(n["verify"], 1), 2),
-        "fallback_flips": int(flips), "kv_dtype": "fp8-e4m3fn + per-page fp32 scales",
-        "note": "includes one plan compile and the device-side view switches",
+        "decode_calls": n_dec, "verify_calls": n_ver,
+        "decode_us_mean": round(1e3 * dt["decode"] / max(n_dec, 1), 2),
+        "verify_us_mean": round(1e3 * dt["verify"] / max(n_ver, 1), 2),
+        "sequences_on_full_context_at_end": flips,
+        "kv_dtype": "fp8-e4m3fn + per-page fp32 scales",
+        "note": "device-resident stream (plan compile, decode/verify calls, device-side "
+                "fallback updates) captured in one HIP graph; effective_gbs uses the graph time",
     }
 
 

@@ -263,6 +263,41 @@ kap_status kap_compact_view(const kap_kv_cache *src, int32_t batch,
                             const kap_kv_cache *dst, int32_t *compact_block_table,
                             void *stream);
 
+/*
+ * kap_fallback_update -- one cycle of the executor's access-mode policy, on
+ * the device, so that a whole proposal / verify stream can be captured in a
+ * HIP graph (Sec. 3.2 "Runtime stability and fallback"; acceptance rate
+ * h = accepted / speculated, Eq. (5); margin condition h > s, Eq. (12)).
+ *
+ * Per sequence b, with s_b = view_tokens[b] / seq_lens[b]:
+ *   reset != 0: history and cycles[b] are cleared; mode[b] = 0 (selected view)
+ *     if plan_status[b] == KAP_PLAN_OK, else 1 (full context); the active
+ *     view row of b is written; accepted is not read (may be NULL).
+ *   reset == 0: the cycle (accepted[b], gamma) enters the last-`window`
+ *     history; cycles[b] += 1; a sequence in mode 0 with cycles[b] >= 2 whose
+ *     window acceptance A / S (sums over the window) satisfies A / S <= s_b
+ *     -- compared exactly as A * seq_lens[b] <= view_tokens[b] * S -- switches
+ *     to mode 1 for good, and its active view row is rewritten.
+ * Active view row: mode 0 copies the plan's row (sel_*); mode 1 is the full
+ * context: view_block_table[b][j] = full_block_table[b][j],
+ * view_logical_block[b][j] = j for j < ceil(seq_lens[b] / 16), and
+ * view_num_blocks[b] = that count. Entries past the row's length are left as
+ * they are.
+ *   history [batch][window][2] int32 (accepted, speculated); cycles, mode
+ *   [batch] int32 -- caller-owned device state kept across calls.
+ *   view_stride >= max(sel_stride, full_stride); 1 <= window <= 64;
+ *   0 <= gamma; accepted[b] is clamped to [0, gamma].
+ */
+kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int32_t gamma,
+                               const int32_t *accepted, const int32_t *view_tokens,
+                               const int32_t *seq_lens, const int32_t *plan_status,
+                               int32_t *history, int32_t *cycles, int32_t *mode,
+                               const int32_t *sel_block_table, const int32_t *sel_logical_block,
+                               const int32_t *sel_num_blocks, int32_t sel_stride,
+                               const int32_t *full_block_table, int32_t full_stride,
+                               int32_t *view_block_table, int32_t *view_logical_block,
+                               int32_t *view_num_blocks, int32_t view_stride, void *stream);
+
 /* Static description of a status code. */
 const char *kap_status_string(kap_status status);
 /* Message of the last failing call on this thread ("" if none). */

@@ -590,4 +590,57 @@ kap_status kap_compact_view(const kap_kv_cache *src, int32_t batch,
   return ok();
 }
 
+kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int32_t gamma,
+                               const int32_t *accepted, const int32_t *view_tokens,
+                               const int32_t *seq_lens, const int32_t *plan_status,
+                               int32_t *history, int32_t *cycles, int32_t *mode,
+                               const int32_t *sel_block_table, const int32_t *sel_logical_block,
+                               const int32_t *sel_num_blocks, int32_t sel_stride,
+                               const int32_t *full_block_table, int32_t full_stride,
+                               int32_t *view_block_table, int32_t *view_logical_block,
+                               int32_t *view_num_blocks, int32_t view_stride, void *stream) {
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (batch > 0x7fffffff / 2) return fail(KAP_ERR_UNSUPPORTED, "batch too large");
+  if (window < 1 || window > 64) return fail(KAP_ERR_INVALID_ARGUMENT, "window %d outside [1, 64]", window);
+  if (gamma < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "gamma < 0");
+  if (sel_stride < 0 || full_stride < 0 || view_stride < sel_stride || view_stride < full_stride)
+    return fail(KAP_ERR_INVALID_ARGUMENT,
+                "need view_stride (%d) >= sel_stride (%d) and full_stride (%d) >= 0", view_stride,
+                sel_stride, full_stride);
+  if (batch == 0) return ok();
+  if ((!reset && !accepted) || !view_tokens || !seq_lens || !plan_status || !history || !cycles ||
+      !mode || !sel_num_blocks || !view_num_blocks)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if ((sel_stride > 0 && (!sel_block_table || !sel_logical_block)) ||
+      (full_stride > 0 && !full_block_table) ||
+      (view_stride > 0 && (!view_block_table || !view_logical_block)))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a table is NULL");
+  kap::FallbackArgs a;
+  a.batch = batch;
+  a.reset = reset != 0;
+  a.window = window;
+  a.gamma = gamma;
+  a.accepted = accepted;
+  a.view_tokens = view_tokens;
+  a.seq_lens = seq_lens;
+  a.plan_status = plan_status;
+  a.history = history;
+  a.cycles = cycles;
+  a.mode = mode;
+  a.sel_bt = sel_block_table;
+  a.sel_lb = sel_logical_block;
+  a.sel_nb = sel_num_blocks;
+  a.sel_stride = sel_stride;
+  a.full_bt = full_block_table;
+  a.full_stride = full_stride;
+  a.view_bt = view_block_table;
+  a.view_lb = view_logical_block;
+  a.view_nb = view_num_blocks;
+  a.view_stride = view_stride;
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_fallback_update(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

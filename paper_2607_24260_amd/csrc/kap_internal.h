@@ -104,7 +104,21 @@ struct CompactArgs {
   int32_t *compact_bt;           // [batch][capacity]
 };
 
+// kap_fallback_update after host validation.
+struct FallbackArgs {
+  int batch, reset, window, gamma;
+  const int32_t *accepted, *view_tokens, *seq_lens, *plan_status;
+  int32_t *history, *cycles, *mode;
+  const int32_t *sel_bt, *sel_lb, *sel_nb;
+  int sel_stride;
+  const int32_t *full_bt;
+  int full_stride;
+  int32_t *view_bt, *view_lb, *view_nb;
+  int view_stride;
+};
+
 hipError_t launch_compile_plan(const PlanArgs &a, hipStream_t s);
+hipError_t launch_fallback_update(const FallbackArgs &a, hipStream_t s);
 hipError_t launch_append_kv(const AppendArgs &a, hipStream_t s);
 hipError_t launch_compact_view(const CompactArgs &a, int grid, hipStream_t s);
 hipError_t launch_attn_generic(const AttnArgs &a, hipStream_t s);

@@ -177,3 +177,90 @@ def run_stream(w, kv, plan: dict, *, window: int = 4, keep_outputs: Optional[set
                 views.apply(policy.mode)
             cycle += 1
     return StreamResult(policy, dec_res, ver_res, np.asarray(acc_all), gammas)
+
+
+class DeviceStream:
+    """The workload's interleaved schedule with the access-mode policy on the
+    device (kap_fallback_update, Sec. 3.2 "Runtime stability and fallback"):
+    a cycle is kernel launches only, all on one stream, so a whole stream can
+    be captured in a HIP graph (``capture``) and replayed. The policy is the
+    one of FallbackPolicy (window, h <= s after the first cycle, sticky,
+    failed plans start on full context); h <= s is compared exactly in
+    integers on the device.
+
+    Accept lengths per cycle come in as device arrays uploaded once (here the
+    seeded draws; the kernel clamps them to gamma). ``plan`` holds the
+    compiled plan tensors; ``plan_call``, if given, recompiles the plan at
+    the start of every stream."""
+
+    def __init__(self, w, kv, plan: dict, *, window: int = 4, plan_call=None, stream=None):
+        import torch
+
+        from . import kap as K
+
+        self.torch = torch
+        dev = kv.device
+        self.stream = stream if stream is not None else torch.cuda.Stream(device=dev)
+        i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32)).to(dev)
+        B = w.batch
+        self.w = w
+        self.plan_call = plan_call
+        self.seq_lens = i32(w.seq_lens)
+        self.fbt = i32(w.full_block_table)
+        cap = plan["view_block_table"].shape[1]
+        stride = max(int(self.fbt.shape[1]), int(cap))
+        self.vbt = torch.zeros((B, stride), dtype=torch.int32, device=dev)
+        self.vlb = torch.zeros((B, stride), dtype=torch.int32, device=dev)
+        self.vnb = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.history = torch.zeros((B, window, 2), dtype=torch.int32, device=dev)
+        self.cycles = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.mode = torch.zeros(B, dtype=torch.int32, device=dev)
+        self.draws = i32(w.accept_draws)                        # [cycles][B]
+        self.gammas = [q.shape[1] - 1 for q in w.q_verify]
+        common = (plan["view_tokens"], self.seq_lens, plan["plan_status"], self.history,
+                  self.cycles, self.mode, plan["view_block_table"], plan["view_logical_block"],
+                  plan["view_num_blocks"], self.fbt, self.vbt, self.vlb, self.vnb)
+        s = self.stream
+        self.reset = K.bind_fallback_update(True, window, 0, None, *common, stream=s)
+        self.update = [K.bind_fallback_update(False, window, g, self.draws[c], *common, stream=s)
+                       for c, g in enumerate(self.gammas)]
+        Hq, D = w.num_q_heads, w.head_dim
+        self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        self.lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        ws = torch.zeros(max(256, K.selected_decode_workspace_bytes(kv, B, stride)),
+                         dtype=torch.uint8, device=dev)
+        self.decode = [K.bind_selected_decode(kv, w.q_decode[i], self.seq_lens, self.vbt,
+                                              self.vlb, self.vnb, stride, w.sm_scale, self.out,
+                                              self.lse, ws, stream=s)
+                       for i in range(w.q_decode.shape[0])]
+        max_len = int(np.max(w.seq_lens))
+        self.ver_out, self.verify = [], []
+        for q in w.q_verify:
+            ql = q.shape[1]
+            ov = torch.empty((B, ql, Hq, D), dtype=torch.float32, device=dev)
+            lv = torch.empty((B, ql, Hq), dtype=torch.float32, device=dev)
+            wv = torch.zeros(max(256, K.verify_workspace_bytes(kv, B, ql, max_len)),
+                             dtype=torch.uint8, device=dev)
+            self.ver_out.append((ov, lv))
+            self.verify.append(K.bind_verify(kv, q, self.seq_lens, self.fbt, max_len, w.sm_scale,
+                                             ov, lv, wv, stream=s))
+
+    def run(self):
+        """Enqueue one whole stream on self.stream (no host synchronisation)."""
+        if self.plan_call is not None:
+            self.plan_call()
+        self.reset()
+        for kind, idx in self.w.schedule:
+            if kind == "decode":
+                self.decode[idx]()
+            else:
+                self.verify[idx]()
+                self.update[idx]()
+
+    def capture(self):
+        """A HIP graph of one whole stream (run)."""
+        torch = self.torch
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=self.stream):
+            self.run()
+        return g

@@ -44,7 +44,7 @@ EXPORTS = (
     "kap_compile_plan", "kap_compile_plan_workspace_bytes",
     "kap_selected_decode", "kap_selected_decode_workspace_bytes",
     "kap_verify", "kap_verify_workspace_bytes",
-    "kap_append_kv", "kap_compact_view",
+    "kap_append_kv", "kap_compact_view", "kap_fallback_update",
     "kap_status_string", "kap_last_error", "kap_abi_version",
 )
 
@@ -113,6 +113,10 @@ def load_library(path: str = LIB_PATH):
     lib.kap_compact_view.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _P, _I32, _P, _I32, ctypes.POINTER(KVCacheStruct),
         _P, _P]
+    lib.kap_fallback_update.restype = _I32
+    lib.kap_fallback_update.argtypes = [
+        _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32,
+        _P, _P, _P, _I32, _P]
     lib.kap_status_string.restype = ctypes.c_char_p
     lib.kap_status_string.argtypes = [_I32]
     lib.kap_last_error.restype = ctypes.c_char_p
@@ -263,6 +267,55 @@ def compact_view(src: KVCache, view_block_table, view_num_blocks, view_capacity:
                                 int(view_capacity), ctypes.byref(dst.struct), _ptr(out),
                                 _stream(stream)))
     return out
+
+
+# --------------------------------------------------------------------------
+# kap_fallback_update
+# --------------------------------------------------------------------------
+
+def bind_fallback_update(reset: bool, window: int, gamma: int, accepted, view_tokens, seq_lens,
+                         plan_status, history, cycles, mode, sel_block_table, sel_logical_block,
+                         sel_num_blocks, full_block_table, view_block_table, view_logical_block,
+                         view_num_blocks, stream=None) -> "BoundCall":
+    """One cycle of the device-side access-mode policy (kap_fallback_update),
+    marshalled once; see kap.h. All arrays int32 on the GPU; history
+    [B][window][2], the tables [B][stride]."""
+    lib = load_library()
+    B = int(seq_lens.shape[0])
+    named = dict(view_tokens=view_tokens, seq_lens=seq_lens, plan_status=plan_status,
+                 cycles=cycles, mode=mode, sel_num_blocks=sel_num_blocks,
+                 view_num_blocks=view_num_blocks)
+    for name, t in named.items():
+        _dev(t, name, torch.int32, 1)
+        if t.shape[0] != B:
+            raise ValueError(f"{name} must have {B} entries")
+    if not reset or accepted is not None:
+        _dev(accepted, "accepted", torch.int32, 1)
+        if accepted.shape[0] != B:
+            raise ValueError(f"accepted must have {B} entries")
+    _dev(history, "history", torch.int32, 3)
+    if tuple(history.shape) != (B, window, 2):
+        raise ValueError(f"history must be {(B, window, 2)}")
+    for name, t in (("sel_block_table", sel_block_table), ("sel_logical_block", sel_logical_block),
+                    ("full_block_table", full_block_table), ("view_block_table", view_block_table),
+                    ("view_logical_block", view_logical_block)):
+        _dev(t, name, torch.int32, 2)
+        if t.shape[0] != B:
+            raise ValueError(f"{name} must have {B} rows")
+    if sel_logical_block.shape != sel_block_table.shape or \
+            view_logical_block.shape != view_block_table.shape:
+        raise ValueError("block and logical-block tables must have the same shape")
+    args = (B, int(bool(reset)), int(window), int(gamma), _ptr(accepted), _ptr(view_tokens),
+            _ptr(seq_lens), _ptr(plan_status), _ptr(history), _ptr(cycles), _ptr(mode),
+            _ptr(sel_block_table), _ptr(sel_logical_block), _ptr(sel_num_blocks),
+            sel_block_table.shape[1], _ptr(full_block_table), full_block_table.shape[1],
+            _ptr(view_block_table), _ptr(view_logical_block), _ptr(view_num_blocks),
+            view_block_table.shape[1], _stream(stream))
+    # not run here: the call updates state (errors surface when it is called)
+    return BoundCall(lib.kap_fallback_update, args,
+                     (accepted, view_tokens, seq_lens, plan_status, history, cycles, mode,
+                      sel_block_table, sel_logical_block, sel_num_blocks, full_block_table,
+                      view_block_table, view_logical_block, view_num_blocks))
 
 
 # --------------------------------------------------------------------------
