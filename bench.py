@@ -477,6 +477,41 @@ def main():
         }
         log(f"kv maintenance: {maint}")
 
+    # full-context decode (the same batch on every page) for the cost model,
+    # and the Top-3 acceptance of 64 gamma = 4 windows over a 151936-token vocabulary
+    phase = accept = None
+    if cfg == 4:
+        from paper_2607_24260_amd import costmodel
+        lblk_f = torch.arange(fbt.shape[1], dtype=torch.int32, device=dev).repeat(B, 1)
+        nb_f = torch.as_tensor(-(-np.asarray(w.seq_lens, dtype=np.int64) // 16)).int().to(dev)
+        ws_f = torch.zeros(max(256, K.selected_decode_workspace_bytes(kvs[0], B, fbt.shape[1])),
+                           dtype=torch.uint8, device=dev)
+        o_f = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        l_f = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        dec_f = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens, fbt, lblk_f, nb_f,
+                                        fbt.shape[1], w.sm_scale, o_f, l_f, ws_f)
+                 for r in range(R)]
+        t_full = time_loop(lambda i: dec_f[i % R](), 27, 3, torch)
+        rep_ = costmodel.measured(q_len - 1, costmodel.expected_acceptance(q_len - 1),
+                                  float(np.mean(s_ratio)), t_dec, t_full, t_ver)
+        phase = {**rep_.as_dict(), "full_context_decode_us": round(t_full * 1e3, 2),
+                 "h_source": "E[min(X, gamma)]/gamma of the recipe's accept law"}
+        log(f"phase: {phase}")
+        aB, aW, aV, nrep = 64, 5, 151936, 4
+        lg = [torch.randn((aB, aW, aV), device=dev).to(torch.bfloat16) for _ in range(nrep)]
+        dr = torch.randint(0, aV, (aB, aW - 1), dtype=torch.int32, device=dev)
+        acc_m = torch.empty(aB, dtype=torch.int32, device=dev)
+        acc_c = torch.empty(aB, dtype=torch.int32, device=dev)
+        acc_ws = torch.zeros(K.load_library().kap_accept_top3_workspace_bytes(aB, aW),
+                             dtype=torch.uint8, device=dev)
+        t_acc = time_loop(lambda i: K.accept_top3(lg[i % nrep], dr, 3, acc_m, acc_c, acc_ws),
+                          40, 3, torch)
+        accept = {"shape": f"{aB} windows x {aW} positions x {aV} vocab, bf16 logits",
+                  "us_per_call": round(t_acc * 1e3, 2),
+                  "gbs": round(aB * aW * aV * 2 / (t_acc * 1e-3) / 1e9, 1)}
+        log(f"accept_top3: {accept}")
+        del lg
+
     ragged = None
     if not args.no_ragged and cfg == 4:
         ragged = ragged_stream(torch, K, dev)
@@ -533,6 +568,8 @@ def main():
             "traffic": counter_traffic("decode_fast_kernel") if cfg == 4 else None,
         },
         "kv_maintenance": maint,
+        "accept_top3": accept,
+        "phase_cost_model": phase,
         "ragged_fp8_stream": ragged,
         "cpu_baseline": cpu,
     }

@@ -298,6 +298,34 @@ kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int
                                int32_t *view_block_table, int32_t *view_logical_block,
                                int32_t *view_num_blocks, int32_t view_stride, void *stream);
 
+/*
+ * kap_accept_top3 -- target-guided tolerant acceptance of a verify window
+ * (Sec. 3.2 "Full-context verification": a proposed token is accepted when it
+ * lies within the full-context verifier's top candidates -- top 3 in the
+ * paper; top_k here).
+ *
+ * The window of sequence b holds the carry token and k = window - 1 proposed
+ * tokens draft_tokens[b][0..k-1]; logits[b][i] are the verifier's logits at
+ * window position i (predicting the token after it). Draft i is accepted
+ * when its rank in logits[b][i] is below top_k, the rank of token d being
+ * the number of tokens j with logit_j > logit_d, or logit_j == logit_d and
+ * j < d (a draft outside [0, vocab) is never accepted). accepted[b] = m, the
+ * number of leading accepted drafts (0..k); carry_token[b] = the argmax of
+ * logits[b][m] (lowest index among equal maxima): the verifier-approved next
+ * token. NaN logits give unspecified results.
+ *   logits [batch][window][vocab] (logits_dtype F32 or BF16, 16-byte
+ *   aligned); draft_tokens [batch][window-1] int32; accepted, carry_token
+ *   [batch] int32. 1 <= window <= 17, 1 <= top_k, 1 <= vocab < 2^30.
+ * Workspace (kap_accept_top3_workspace_bytes): per-row counters that must be
+ * zero at call start and are left zero (allocate it zero-filled once).
+ */
+kap_status kap_accept_top3(int32_t batch, int32_t window, int32_t vocab, const void *logits,
+                           kap_dtype logits_dtype, const int32_t *draft_tokens, int32_t top_k,
+                           int32_t *accepted, int32_t *carry_token, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+size_t kap_accept_top3_workspace_bytes(int32_t batch, int32_t window);
+
 /* Static description of a status code. */
 const char *kap_status_string(kap_status status);
 /* Message of the last failing call on this thread ("" if none). */

@@ -20,6 +20,8 @@ Systems" (arXiv 2607.24260). What is computed, and where it is defined:
   workspace (Alg. 1, AssignCompactSlots / BuildBlockTable): placing new
   tokens into their KV slots, and copying a view's pages into a compact
   workspace of fixed capacity.
+* ``accept_top_k`` -- Sec. 3.2 target-guided tolerant verification (the
+  Top-3 rule): accepted prefix length and the verifier's carry token.
 * ``lse_merge`` -- the exact softmax identity used to combine attention over
   disjoint key sets (a standard identity, not stated in the paper).
 * ``e4m3fn_to_f64`` / ``bf16_to_f64`` -- decoding of stored KV bits (OCP 8-bit
@@ -480,3 +482,43 @@ def compact_view(pool: KVPool, view_block_table, view_num_blocks, capacity: int)
                 sc[dst] = pool.scales[p]
             table[b, j] = dst
     return KVPool(k, v, pool.dtype, sc), table
+
+
+# --------------------------------------------------------------------------
+# Tolerant acceptance of a verify window
+# --------------------------------------------------------------------------
+
+def token_rank(row: np.ndarray, d: int) -> int:
+    """Rank of token d in a logits row: the number of tokens that come before
+    it when the row is ordered by logit (largest first), ties broken by the
+    lower token index."""
+    x = np.asarray(row, dtype=np.float64)
+    idx = np.arange(len(x))
+    return int(np.sum((x > x[d]) | ((x == x[d]) & (idx < d))))
+
+
+def accept_top_k(logits: np.ndarray, drafts: np.ndarray, top_k: int = 3):
+    """Sec. 3.2 ("Full-context verification"): the verifier accepts a proposed
+    token when it lies within its top candidates under the full context (the
+    paper's Top-3 rule); the accepted count m is the number of leading
+    accepted proposals, and the verifier's next (carry) token is its choice at
+    position m.
+
+    logits [B][window][vocab]: the verifier's logits at the window positions;
+    drafts [B][window-1]: proposed tokens (draft i is scored in row i).
+    Returns (m [B], carry [B]); carry = argmax of row m (lowest index among
+    equal maxima). A draft outside [0, vocab) is never accepted."""
+    logits = np.asarray(logits, dtype=np.float64)
+    B, Wn, V = logits.shape
+    m = np.zeros(B, dtype=np.int64)
+    carry = np.zeros(B, dtype=np.int64)
+    for b in range(B):
+        i = 0
+        while i < Wn - 1:
+            d = int(drafts[b][i])
+            if not 0 <= d < V or token_rank(logits[b, i], d) >= top_k:
+                break
+            i += 1
+        m[b] = i
+        carry[b] = int(np.argmax(logits[b, i]))
+    return m, carry

@@ -643,4 +643,56 @@ kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int
   return ok();
 }
 
+// Workspace of kap_accept_top3: [row_best u64 x rows][row_count i32 x rows].
+static size_t accept_ws(int batch, int window, size_t *count_off) {
+  const size_t rows = (size_t)batch * window;
+  const size_t best = round_up(rows * sizeof(unsigned long long), 256);
+  if (count_off) *count_off = best;
+  return best + round_up(rows * sizeof(int32_t), 256);
+}
+
+size_t kap_accept_top3_workspace_bytes(int32_t batch, int32_t window) {
+  if (batch <= 0 || window < 1 || window > 17) return 0;
+  return accept_ws(batch, window, nullptr);
+}
+
+kap_status kap_accept_top3(int32_t batch, int32_t window, int32_t vocab, const void *logits,
+                           kap_dtype logits_dtype, const int32_t *draft_tokens, int32_t top_k,
+                           int32_t *accepted, int32_t *carry_token, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (window < 1 || window > 17) return fail(KAP_ERR_INVALID_ARGUMENT, "window %d outside [1, 17]", window);
+  if (vocab < 1 || vocab >= (1 << 30)) return fail(KAP_ERR_INVALID_ARGUMENT, "vocab %d outside [1, 2^30)", vocab);
+  if (top_k < 1) return fail(KAP_ERR_INVALID_ARGUMENT, "top_k < 1");
+  if (logits_dtype != KAP_DT_F32 && logits_dtype != KAP_DT_BF16)
+    return fail(KAP_ERR_UNSUPPORTED, "logits must be F32 or BF16");
+  if (batch == 0) return ok();
+  if ((long long)batch * window > 65535)
+    return fail(KAP_ERR_UNSUPPORTED, "batch * window > 65535");
+  if (!logits || !accepted || !carry_token || (window > 1 && !draft_tokens))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (!aligned(logits, 16)) return fail(KAP_ERR_INVALID_ARGUMENT, "logits must be 16-byte aligned");
+  size_t count_off = 0;
+  const size_t need = accept_ws(batch, window, &count_off);
+  if (!workspace || workspace_bytes < need)
+    return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
+  if (!aligned(workspace, 256)) return fail(KAP_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  kap::AcceptArgs a;
+  a.batch = batch;
+  a.window = window;
+  a.vocab = vocab;
+  a.top_k = top_k;
+  a.f32 = logits_dtype == KAP_DT_F32;
+  a.logits = logits;
+  a.drafts = draft_tokens;
+  a.accepted = accepted;
+  a.carry = carry_token;
+  a.row_best = static_cast<unsigned long long *>(workspace);
+  a.row_count = reinterpret_cast<int32_t *>(static_cast<char *>(workspace) + count_off);
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_accept_top3(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"

@@ -117,7 +117,19 @@ struct FallbackArgs {
   int view_stride;
 };
 
+// kap_accept_top3 after host validation.
+constexpr int kAcceptChunk = 16384;  // vocabulary tokens per row workgroup
+struct AcceptArgs {
+  int batch, window, vocab, top_k, f32;
+  const void *logits;            // [batch][window][vocab]
+  const int32_t *drafts;         // [batch][window - 1]
+  int32_t *accepted, *carry;     // [batch]
+  int32_t *row_count;            // workspace [batch * window], zero between calls
+  unsigned long long *row_best;  // workspace [batch * window], zero between calls
+};
+
 hipError_t launch_compile_plan(const PlanArgs &a, hipStream_t s);
+hipError_t launch_accept_top3(const AcceptArgs &a, hipStream_t s);
 hipError_t launch_fallback_update(const FallbackArgs &a, hipStream_t s);
 hipError_t launch_append_kv(const AppendArgs &a, hipStream_t s);
 hipError_t launch_compact_view(const CompactArgs &a, int grid, hipStream_t s);

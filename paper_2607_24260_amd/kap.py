@@ -45,6 +45,7 @@ EXPORTS = (
     "kap_selected_decode", "kap_selected_decode_workspace_bytes",
     "kap_verify", "kap_verify_workspace_bytes",
     "kap_append_kv", "kap_compact_view", "kap_fallback_update",
+    "kap_accept_top3", "kap_accept_top3_workspace_bytes",
     "kap_status_string", "kap_last_error", "kap_abi_version",
 )
 
@@ -117,6 +118,10 @@ def load_library(path: str = LIB_PATH):
     lib.kap_fallback_update.argtypes = [
         _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32,
         _P, _P, _P, _I32, _P]
+    lib.kap_accept_top3.restype = _I32
+    lib.kap_accept_top3.argtypes = [_I32, _I32, _I32, _P, _I32, _P, _I32, _P, _P, _P, _SZ, _P]
+    lib.kap_accept_top3_workspace_bytes.restype = _SZ
+    lib.kap_accept_top3_workspace_bytes.argtypes = [_I32, _I32]
     lib.kap_status_string.restype = ctypes.c_char_p
     lib.kap_status_string.argtypes = [_I32]
     lib.kap_last_error.restype = ctypes.c_char_p
@@ -316,6 +321,38 @@ def bind_fallback_update(reset: bool, window: int, gamma: int, accepted, view_to
                      (accepted, view_tokens, seq_lens, plan_status, history, cycles, mode,
                       sel_block_table, sel_logical_block, sel_num_blocks, full_block_table,
                       view_block_table, view_logical_block, view_num_blocks))
+
+
+# --------------------------------------------------------------------------
+# kap_accept_top3
+# --------------------------------------------------------------------------
+
+def accept_top3(logits, draft_tokens, top_k: int = 3, accepted=None, carry=None,
+                workspace=None, stream=None):
+    """Tolerant acceptance of verify windows: logits [B][window][vocab]
+    (float32 / bfloat16), draft_tokens [B][window-1] int32. Returns
+    (accepted [B], carry_token [B]) int32 tensors; see kap.h."""
+    lib = load_library()
+    _dev(logits, "logits", None, 3)
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("logits must be float32 or bfloat16")
+    B, Wn, V = logits.shape
+    _dev(draft_tokens, "draft_tokens", torch.int32, 2)
+    if tuple(draft_tokens.shape) != (B, Wn - 1):
+        raise ValueError(f"draft_tokens must be {(B, Wn - 1)}")
+    dev = logits.device
+    if accepted is None:
+        accepted = torch.empty(B, dtype=torch.int32, device=dev)
+    if carry is None:
+        carry = torch.empty(B, dtype=torch.int32, device=dev)
+    _dev(accepted, "accepted", torch.int32, 1)
+    _dev(carry, "carry", torch.int32, 1)
+    workspace, have = _workspace(int(lib.kap_accept_top3_workspace_bytes(B, Wn)), dev, workspace)
+    dt = KAP_DT_F32 if logits.dtype == torch.float32 else KAP_DT_BF16
+    _check(lib.kap_accept_top3(B, Wn, V, _ptr(logits), dt, _ptr(draft_tokens), int(top_k),
+                               _ptr(accepted), _ptr(carry), _ptr(workspace), have,
+                               _stream(stream)))
+    return accepted, carry
 
 
 # --------------------------------------------------------------------------

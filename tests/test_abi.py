@@ -23,7 +23,7 @@ def lib():
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kap_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(kap_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_boundary():
@@ -166,3 +166,15 @@ def test_compact_view_rejects_bad_arguments(lib):
     assert comp(kv_struct(num_pages=64, Hkv=4)) == K.KAP_ERR_INVALID_ARGUMENT    # geometry
     assert comp(kv_struct(num_pages=64), table=None) == K.KAP_ERR_INVALID_ARGUMENT
     assert comp(kv_struct(num_pages=0), batch=0) == K.KAP_OK                     # no-op
+
+
+def test_accept_top3_rejects_bad_arguments(lib):
+    acc = lambda B=2, Wn=5, V=100, dt=K.KAP_DT_BF16, top_k=3, ws=FAKE, ws_bytes=1 << 20: \
+        lib.kap_accept_top3(B, Wn, V, FAKE, dt, FAKE, top_k, FAKE, FAKE, ws, ws_bytes, None)
+    assert acc(Wn=0) == K.KAP_ERR_INVALID_ARGUMENT
+    assert acc(Wn=18) == K.KAP_ERR_INVALID_ARGUMENT
+    assert acc(top_k=0) == K.KAP_ERR_INVALID_ARGUMENT
+    assert acc(dt=K.KAP_DT_FP8_E4M3FN) == K.KAP_ERR_UNSUPPORTED
+    assert acc(ws_bytes=16) == K.KAP_ERR_WORKSPACE_TOO_SMALL
+    assert acc(B=0) == K.KAP_OK
+    assert lib.kap_accept_top3_workspace_bytes(64, 9) == 576 * 8 + 576 * 4   # 576 rows: u64 maxima, then int32 counts
