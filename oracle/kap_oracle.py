@@ -160,6 +160,7 @@ class Plan:
     view_tokens: int            # visible tokens of the selected pages
     spans_taken: int
     span_selected: list         # per input span: 1 if selected, else 0
+    token_masks: Optional[list] = None   # token-granular plans: visible-token bits per view page
 
 
 def _pages_of(x: int, e: int) -> set:
@@ -238,22 +239,75 @@ def compile_plan_one(seq_len: int, fbt_row: Sequence[int], starts: Sequence[int]
     return Plan(PLAN_OK, lblk, vbt, len(lblk), used, taken, flags)
 
 
+def compile_plan_tokens_one(seq_len: int, fbt_row: Sequence[int], starts: Sequence[int],
+                            lens: Sequence[int], priors: Sequence[float], prefix: int,
+                            suffix: int, budget: int, policy: int, num_pages: int,
+                            capacity: int) -> Plan:
+    """``compile_plan_one`` with token-granular visibility (the visibility mask
+    of Sec. 3.1 at token resolution): the selection, the budget and the
+    mandatory prefix / suffix are counted in tokens, a span costs the tokens
+    it adds, and the view lists every logical page holding a visible token,
+    with a 16-bit mask of its visible tokens (bit t = token t of the page).
+    Ranking, the SKIP / STOP rule and the status codes are as for pages."""
+    n = len(starts)
+    L = int(seq_len)
+    fail = Plan(PLAN_OK, [], [], 0, 0, 0, [0] * n, [])
+    if L < 1 or -(-L // PAGE) > len(fbt_row):
+        fail.status = PLAN_BAD_LENGTH
+        return fail
+    if any(math.isnan(float(p)) for p in priors):
+        fail.status = PLAN_BAD_SCORE
+        return fail
+
+    sel = set(range(0, min(max(prefix, 0), L)))
+    sel |= set(range(max(0, L - max(suffix, 1)), L))
+    order = sorted(range(n), key=lambda i: (-float(priors[i]), int(starts[i]), i))
+    taken = 0
+    flags = [0] * n
+    for i in order:
+        x = max(0, int(starts[i]))
+        e = min(L, int(starts[i]) + int(lens[i]))
+        if e <= x:
+            continue
+        new = set(range(x, e)) - sel
+        if len(sel) + len(new) <= budget:
+            sel |= new
+            taken += 1
+            flags[i] = 1
+        elif policy == SELECT_STOP:
+            break
+
+    lblk = sorted({t // PAGE for t in sel})
+    if len(lblk) > capacity:
+        fail.status = PLAN_OVER_CAPACITY
+        return fail
+    vbt = [int(fbt_row[j]) for j in lblk]
+    if any(p < 0 or p >= num_pages for p in vbt):
+        fail.status = PLAN_BAD_PAGE
+        return fail
+    masks = [sum(1 << (t - PAGE * j) for t in sel if t // PAGE == j) for j in lblk]
+    return Plan(PLAN_OK, lblk, vbt, len(lblk), len(sel), taken, flags, masks)
+
+
 def compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len,
                  span_prior, prefix, suffix, budget, policy, num_pages,
-                 capacity) -> list:
+                 capacity, token_granular: bool = False) -> list:
     """Batched ``compile_plan_one`` over CSR span arrays; returns a list of Plan.
 
     Sequence b owns spans span_offsets[b] .. span_offsets[b+1]-1. Malformed CSR
-    bounds give PLAN_BAD_SPANS for that sequence.
+    bounds give PLAN_BAD_SPANS for that sequence. ``token_granular`` selects
+    ``compile_plan_tokens_one``.
     """
     out = []
     total = len(span_start)
     for b in range(len(seq_lens)):
         lo, hi = int(span_offsets[b]), int(span_offsets[b + 1])
         if lo < 0 or hi < lo or hi > total:
-            out.append(Plan(PLAN_BAD_SPANS, [], [], 0, 0, 0, []))
+            out.append(Plan(PLAN_BAD_SPANS, [], [], 0, 0, 0, [],
+                            [] if token_granular else None))
             continue
-        out.append(compile_plan_one(
+        one = compile_plan_tokens_one if token_granular else compile_plan_one
+        out.append(one(
             int(seq_lens[b]), full_block_table[b], span_start[lo:hi],
             span_len[lo:hi], span_prior[lo:hi], int(prefix[b]), int(suffix[b]),
             int(budget[b]), policy, num_pages, capacity))
@@ -289,7 +343,8 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, n_visible: Sequence[int]
     return o, lse
 
 
-def _view_tokens(pool: KVPool, g: int, seq_len: int, pages, lblks, skip_invalid: bool = True):
+def _view_tokens(pool: KVPool, g: int, seq_len: int, pages, lblks, skip_invalid: bool = True,
+                 masks=None):
     """K and V of the visible tokens of a list of (physical, logical) pages.
 
     A view entry whose page id lies outside the pool contributes no keys (the
@@ -297,28 +352,34 @@ def _view_tokens(pool: KVPool, g: int, seq_len: int, pages, lblks, skip_invalid:
     KAP_PLAN_BAD_PAGE)."""
     pages = np.asarray(pages, dtype=np.int64)
     lblks = np.asarray(lblks, dtype=np.int64)
+    masks = (np.full(len(pages), 0xFFFF, dtype=np.int64) if masks is None
+             else np.asarray(masks, dtype=np.int64))
     if skip_invalid:
         ok = (pages >= 0) & (pages < pool.k_pages.shape[0])
-        pages, lblks = pages[ok], lblks[ok]
+        pages, lblks, masks = pages[ok], lblks[ok], masks[ok]
     if len(pages) == 0:
         D = pool.v_pages.shape[2]
         return np.zeros((0, D)), np.zeros((0, D))
     nvalid = np.clip(seq_len - PAGE * lblks, 0, PAGE)
-    mask = np.arange(PAGE)[None, :] < nvalid[:, None]         # [n][PAGE]
+    t = np.arange(PAGE)[None, :]
+    mask = (t < nvalid[:, None]) & (((masks[:, None] >> t) & 1) == 1)   # [n][PAGE]
     k = pool.keys(pages, g)[mask]
     v = pool.values(pages, g)[mask]
     return k, v
 
 
 def selected_decode(pool: KVPool, q: np.ndarray, seq_lens, view_block_table,
-                    view_logical_block, view_num_blocks, sm_scale: float):
+                    view_logical_block, view_num_blocks, sm_scale: float,
+                    view_token_mask=None):
     """One proposal step over the selected-KV view (Sec. 3.2, q_prop = 1).
 
     q: [B][Hq][D] (any float dtype; promoted to fp64). Sequence b sees the
     first view_num_blocks[b] view blocks; block k is physical page
     view_block_table[b][k] holding logical page view_logical_block[b][k], whose
     tokens below seq_lens[b] are visible. Query head h uses KV head
-    h // (Hq / Hkv). Returns o [B][Hq][D] and lse [B][Hq] in float64.
+    h // (Hq / Hkv). With ``view_token_mask`` [B][cap] (token-granular
+    plans), token t of view block k is visible only if bit t of its mask is
+    set. Returns o [B][Hq][D] and lse [B][Hq] in float64.
     """
     q = np.asarray(q, dtype=np.float64)
     B, Hq, D = q.shape
@@ -330,8 +391,9 @@ def selected_decode(pool: KVPool, q: np.ndarray, seq_lens, view_block_table,
         nb = int(view_num_blocks[b])
         pages = np.asarray(view_block_table[b])[:nb]
         lblks = np.asarray(view_logical_block[b])[:nb]
+        masks = None if view_token_mask is None else np.asarray(view_token_mask[b])[:nb]
         for g in range(Hkv):
-            k, v = _view_tokens(pool, g, int(seq_lens[b]), pages, lblks)
+            k, v = _view_tokens(pool, g, int(seq_lens[b]), pages, lblks, masks=masks)
             rows = q[b, g * G:(g + 1) * G]
             ob, lb = attend(rows, k, v, [k.shape[0]] * G, sm_scale)
             o[b, g * G:(g + 1) * G] = ob

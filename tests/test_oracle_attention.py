@@ -391,7 +391,7 @@ def test_planted_last_page_count_is_caught(monkeypatch):
 
     def patch(m, pool):
         m.setattr(O, "_view_tokens",
-                  lambda pool_, g, L, pages, lblks: orig(pool_, g, L + 1, pages, lblks))
+                  lambda pool_, g, L, pages, lblks, **kw: orig(pool_, g, L + 1, pages, lblks, **kw))
     assert _decode_mismatch(monkeypatch, patch) > 1e-3
 
 
