@@ -171,6 +171,43 @@ size_t kap_compile_plan_workspace_bytes(int32_t batch, int32_t num_spans,
                                         int32_t fbt_stride);
 
 /*
+ * kap_compile_plan_masked -- kap_compile_plan with the visibility mask of
+ * Sec. 3.1 kept at token resolution: a span is exposed as its tokens, not as
+ * whole pages.
+ *
+ * Per sequence b, as kap_compile_plan except that selection is over token
+ * sets:
+ *  1. Mandatory tokens: [0, min(prefix,L)) and [max(0, L - max(suffix,1)), L).
+ *     used = their number.
+ *  2. Ranking as kap_compile_plan.
+ *  3. A non-empty clipped span costs its tokens not yet visible; it is taken
+ *     iff used + cost <= budget_tokens[b] (then its tokens become visible),
+ *     else skipped or, with KAP_SELECT_STOP, selection ends.
+ *  4. The view lists, ascending, every logical page holding a visible token;
+ *     view_token_mask[b][k] (uint32, bits 16..31 zero) has bit t set iff token
+ *     16*view_logical_block[b][k] + t is visible. view_tokens[b] = used.
+ * Status codes, outputs and workspace are those of kap_compile_plan; the
+ * extra output view_token_mask is [batch][view_capacity] (entries past
+ * view_num_blocks[b] are left unchanged; may be NULL only if
+ * view_capacity == 0).
+ * Limits: fbt_stride <= 16384 pages per sequence (262144 tokens).
+ * Result is unique and bit-for-bit deterministic.
+ */
+kap_status kap_compile_plan_masked(int32_t batch, const int32_t *seq_lens,
+                                   const int32_t *full_block_table, int32_t fbt_stride,
+                                   const int32_t *span_offsets, int32_t num_spans,
+                                   const int32_t *span_start, const int32_t *span_len,
+                                   const float *span_prior, const int32_t *prefix_tokens,
+                                   const int32_t *suffix_tokens, const int32_t *budget_tokens,
+                                   kap_select_policy policy, int64_t num_pages,
+                                   int32_t view_capacity, int32_t *view_block_table,
+                                   int32_t *view_logical_block, uint32_t *view_token_mask,
+                                   int32_t *view_num_blocks, int32_t *view_tokens,
+                                   int32_t *spans_taken, int32_t *plan_status,
+                                   int32_t *span_selected, void *workspace,
+                                   size_t workspace_bytes, void *stream);
+
+/*
  * kap_selected_decode -- one proposal step (q_prop = 1) over the selected-KV
  * view (Sec. 3.2, "Selected-KV proposal").
  *
@@ -197,6 +234,24 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
 
 size_t kap_selected_decode_workspace_bytes(const kap_kv_cache *kv, int32_t batch,
                                            int32_t max_view_blocks, int32_t num_splits);
+
+/*
+ * kap_selected_decode_masked -- kap_selected_decode over a token-granular
+ * view (the output of kap_compile_plan_masked): token t of view block k is
+ * visible iff it is visible to kap_selected_decode AND bit t of
+ * view_token_mask[b][k] is set.
+ *   view_token_mask [batch][view_stride] uint32, laid out like the view
+ *   tables (may be NULL only if max_view_blocks == 0). Every other argument,
+ *   the workspace (kap_selected_decode_workspace_bytes) and the errors are
+ *   those of kap_selected_decode.
+ */
+kap_status kap_selected_decode_masked(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                      const int32_t *seq_lens, const int32_t *view_block_table,
+                                      const int32_t *view_logical_block,
+                                      const uint32_t *view_token_mask, int32_t view_stride,
+                                      const int32_t *view_num_blocks, int32_t max_view_blocks,
+                                      float sm_scale, int32_t num_splits, float *out, float *lse,
+                                      void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * kap_verify -- full-context verification attention of the q_len = k+1

@@ -67,8 +67,10 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(AttnArgs a) {
     const int page = a.block_table[(size_t)b * a.bt_stride + k];
     const int lb = a.logical_block ? a.logical_block[(size_t)b * a.bt_stride + k] : k;
     const long long pos = (long long)lb * kPage + tok;
+    const bool shown =
+        !a.token_mask || ((a.token_mask[(size_t)b * a.bt_stride + k] >> tok) & 1u);
     float z = -INFINITY;
-    if (page >= 0 && page < a.num_pages && pos < limit && pos < L) {
+    if (shown && page >= 0 && page < a.num_pages && pos < limit && pos < L) {
       // K page tile: [D/8 chunks][16 tokens][8 dims]
       const size_t kbase = ((size_t)page * a.Hkv + g) * kPage * D + (size_t)tok * 8;
       float acc = 0.f;

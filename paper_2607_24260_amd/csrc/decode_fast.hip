@@ -152,7 +152,7 @@ __device__ __forceinline__ void v_floats(const PageRegs<KV> &r, float vv[4][8]) 
   }
 }
 
-template <int KV, int RING, bool BALANCED>
+template <int KV, int RING, bool BALANCED, bool MASKED>
 __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   __shared__ float pbuf[kWaves][64];
   __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
@@ -195,14 +195,17 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   // with row stride 0, so entry 0 of the row is always readable.)
   const int last_entry = max(a.max_blocks - 1, 0);
   int raw_pg[RING], raw_lb[RING];
+  uint32_t raw_mk[RING];
   auto first_entries = [&](const WorkItem &x) {
     const int32_t *bt = a.block_table + (size_t)x.b * a.bt_stride;
     const int32_t *lb = a.logical_block + (size_t)x.b * a.bt_stride;
+    const uint32_t *mk = MASKED ? a.token_mask + (size_t)x.b * a.bt_stride : nullptr;
 #pragma unroll
     for (int j = 0; j < RING; ++j) {
       const int kk = min(x.split * kWaves + wave + x.n_split * kWaves * j, last_entry);
       raw_pg[j] = bt[kk];
       raw_lb[j] = lb[kk];
+      raw_mk[j] = MASKED ? mk[kk] : 0xFFFFu;
     }
   };
   int L, nb;
@@ -227,10 +230,12 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   const int u = split * kWaves + wave;
   const int32_t *vbt = a.block_table + (size_t)b * a.bt_stride;
   const int32_t *vlb = a.logical_block + (size_t)b * a.bt_stride;
-  auto table_read = [&](int i, int &raw_page, int &raw_lblk) {
+  const uint32_t *vmk = MASKED ? a.token_mask + (size_t)b * a.bt_stride : nullptr;
+  auto table_read = [&](int i, int &raw_page, int &raw_lblk, uint32_t &raw_mask) {
     const int kk = min(u + nw * i, last_entry);
     raw_page = vbt[kk];
     raw_lblk = vlb[kk];
+    raw_mask = MASKED ? vmk[kk] : 0xFFFFu;
   };
 
   // query slices of the four heads, as bf16 pairs matching the K slice
@@ -258,24 +263,29 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   const int n_my = u < nb ? div_small(nb - 1 - u, nw) + 1 : 0;
 
   // The i-th view entry of this wavefront -> its page (0 for an invalid id)
-  // and number of visible tokens (0 if the id is invalid, the block lies past
-  // the sequence, or i is past this wavefront's entries).
-  auto validate = [&](int i, int raw_page, int raw_lblk, int &page, int &nvalid) {
+  // and its visible tokens as a 16-bit mask, bit t = token t (none if the id
+  // is invalid, the block lies past the sequence, or i is past this
+  // wavefront's entries): tokens below the sequence length, and with a token
+  // mask only those whose bit is set.
+  auto validate = [&](int i, int raw_page, int raw_lblk, uint32_t raw_mask, int &page,
+                      uint32_t &vis) {
     const long long rem = (long long)L - (long long)raw_lblk * kPage;
-    nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
+    const int nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
+    vis = (0xFFFFu >> (kPage - nvalid)) & raw_mask;
     page = raw_page;
     if (page < 0 || (int64_t)page >= a.num_pages || i >= n_my) {
-      nvalid = 0;
+      vis = 0u;
       page = 0;
     }
   };
-  auto page_info = [&](int i, int &page, int &nvalid) {   // used only when n_my > 0
+  auto page_info = [&](int i, int &page, uint32_t &vis) {   // used only when n_my > 0
     int rp, rl;
-    table_read(i, rp, rl);
-    validate(i, rp, rl, page, nvalid);
+    uint32_t rm;
+    table_read(i, rp, rl, rm);
+    validate(i, rp, rl, rm, page, vis);
   };
 
-  auto process = [&](const PageRegs<KV> &cur, int page, int nvalid) {
+  auto process = [&](const PageRegs<KV> &cur, int page, uint32_t vis) {
     float ksc = a.scale_log2, vsc = 1.f;
     if constexpr (KV == kFP8) {
       ksc *= cur.sc.x;
@@ -302,7 +312,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     keep1 += dpp<kQuadXor1>(send1);
     float s = o2 ? keep1 : keep0;
     s += dpp<kQuadXor2>(o2 ? keep0 : keep1);
-    s = (t < nvalid) ? s * ksc : -INFINITY;
+    s = ((vis >> t) & 1u) ? s * ksc : -INFINITY;
 
     // ---- online softmax ------------------------------------------------------
     float pm = fmaxf(s, dpp<kRowRor4>(s));
@@ -333,10 +343,10 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     // ---- o += p V --------------------------------------------------------------
     float vv[4][8];
     v_floats<KV>(cur, vv);
-    if (nvalid < kPage) {
+    if (vis != 0xFFFFu) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const bool ok = hf * 8 + j < nvalid;
+        const bool ok = (vis >> (hf * 8 + j)) & 1u;
 #pragma unroll
         for (int i = 0; i < 4; ++i) vv[i][j] = ok ? vv[i][j] : 0.f;
       }
@@ -365,11 +375,12 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   // would merge a just-issued load into the loop header's wait and drain the
   // ring every round -- and the remaining pages are processed after it.
   PageRegs<KV> r[RING];
-  int pg[RING], nv[RING];
+  int pg[RING];
+  uint32_t nv[RING];
 #pragma unroll
   for (int j = 0; j < RING; ++j) {
-    validate(j, raw_pg[j], raw_lb[j], pg[j], nv[j]);
-    load_page<KV>(r[j], a, pg[j], g, lane, nv[j] > 0);
+    validate(j, raw_pg[j], raw_lb[j], raw_mk[j], pg[j], nv[j]);
+    load_page<KV>(r[j], a, pg[j], g, lane, nv[j] != 0u);
   }
   const int full = n_my - n_my % RING;
   for (int i = 0; i < full; i += RING) {
@@ -377,7 +388,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     for (int j = 0; j < RING; ++j) {
       process(r[j], pg[j], nv[j]);
       page_info(i + j + RING, pg[j], nv[j]);
-      load_page<KV>(r[j], a, pg[j], g, lane, nv[j] > 0);
+      load_page<KV>(r[j], a, pg[j], g, lane, nv[j] != 0u);
     }
   }
 #pragma unroll
@@ -454,13 +465,22 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   if (last_arrival(a, b, g, n_split, &s_flag)) merge_rows(a, b, g, 4, wi.slot0, n_split);
 }
 
+template <int KV, int RING, bool MASKED>
+void launch_mode(const AttnArgs &a, hipStream_t s) {
+  if (a.ragged)
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, true, MASKED>), dim3(a.n_split), dim3(256),
+                       0, s, a);
+  else
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, false, MASKED>),
+                       dim3(a.n_split, a.Hkv, a.batch), dim3(256), 0, s, a);
+}
+
 template <int KV, int RING>
 hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
-  if (a.ragged)
-    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, true>), dim3(a.n_split), dim3(256), 0, s, a);
+  if (a.token_mask)
+    launch_mode<KV, RING, true>(a, s);
   else
-    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, false>), dim3(a.n_split, a.Hkv, a.batch),
-                       dim3(256), 0, s, a);
+    launch_mode<KV, RING, false>(a, s);
   return hipGetLastError();
 }
 
@@ -477,9 +497,9 @@ int decode_fast_blocks_per_cu(int kv_type) {
   const hipError_t e =
       kv_type == kFP8
           ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &nb, decode_fast_kernel<kFP8, kRingFP8, true>, 256, 0)
+                &nb, decode_fast_kernel<kFP8, kRingFP8, true, false>, 256, 0)
           : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &nb, decode_fast_kernel<kBF16, kRingBF16, true>, 256, 0);
+                &nb, decode_fast_kernel<kBF16, kRingBF16, true, false>, 256, 0);
   return e == hipSuccess ? nb : 0;
 }
 

@@ -293,16 +293,18 @@ size_t kap_compile_plan_workspace_bytes(int32_t batch, int32_t num_spans, int32_
   return num_spans > 0 ? round_up((size_t)num_spans * sizeof(int32_t), 256) : 0;
 }
 
-kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens, const int32_t *full_block_table,
-                            int32_t fbt_stride, const int32_t *span_offsets, int32_t num_spans,
-                            const int32_t *span_start, const int32_t *span_len,
-                            const float *span_prior, const int32_t *prefix_tokens,
-                            const int32_t *suffix_tokens, const int32_t *budget_tokens,
-                            kap_select_policy policy, int64_t num_pages, int32_t view_capacity,
-                            int32_t *view_block_table, int32_t *view_logical_block,
-                            int32_t *view_num_blocks, int32_t *view_tokens, int32_t *spans_taken,
-                            int32_t *plan_status, int32_t *span_selected, void *workspace,
-                            size_t workspace_bytes, void *stream) {
+static kap_status compile_plan(int32_t batch, const int32_t *seq_lens,
+                               const int32_t *full_block_table, int32_t fbt_stride,
+                               const int32_t *span_offsets, int32_t num_spans,
+                               const int32_t *span_start, const int32_t *span_len,
+                               const float *span_prior, const int32_t *prefix_tokens,
+                               const int32_t *suffix_tokens, const int32_t *budget_tokens,
+                               kap_select_policy policy, int64_t num_pages, int32_t view_capacity,
+                               int32_t *view_block_table, int32_t *view_logical_block,
+                               uint32_t *view_token_mask, bool token_mode,
+                               int32_t *view_num_blocks, int32_t *view_tokens,
+                               int32_t *spans_taken, int32_t *plan_status, int32_t *span_selected,
+                               void *workspace, size_t workspace_bytes, void *stream) {
   if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
   if (num_spans < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "num_spans < 0");
   if (view_capacity < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "view_capacity < 0");
@@ -310,8 +312,9 @@ kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens, const int32_
   if (policy != KAP_SELECT_SKIP && policy != KAP_SELECT_STOP)
     return fail(KAP_ERR_INVALID_ARGUMENT, "unknown selection policy %d", policy);
   if (fbt_stride < 1) return fail(KAP_ERR_INVALID_ARGUMENT, "fbt_stride < 1");
-  if (fbt_stride > kap::kMaxPlanPages)
-    return fail(KAP_ERR_UNSUPPORTED, "fbt_stride %d exceeds %d pages", fbt_stride, kap::kMaxPlanPages);
+  const int max_pages = token_mode ? kap::kMaxTokenPlanPages : kap::kMaxPlanPages;
+  if (fbt_stride > max_pages)
+    return fail(KAP_ERR_UNSUPPORTED, "fbt_stride %d exceeds %d pages", fbt_stride, max_pages);
   if (batch == 0) return ok();
   if (!seq_lens || !full_block_table || !span_offsets || !prefix_tokens || !suffix_tokens ||
       !budget_tokens || !view_num_blocks || !view_tokens || !spans_taken || !plan_status)
@@ -320,6 +323,8 @@ kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens, const int32_
     return fail(KAP_ERR_INVALID_ARGUMENT, "span arrays are NULL");
   if (view_capacity > 0 && (!view_block_table || !view_logical_block))
     return fail(KAP_ERR_INVALID_ARGUMENT, "view tables are NULL");
+  if (token_mode && view_capacity > 0 && !view_token_mask)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "view_token_mask is NULL");
   const size_t need = kap_compile_plan_workspace_bytes(batch, num_spans, fbt_stride);
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
@@ -348,10 +353,51 @@ kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens, const int32_
   a.status = plan_status;
   a.span_selected = span_selected;
   a.perm = static_cast<int32_t *>(workspace);
+  a.token_mode = token_mode ? 1 : 0;
+  a.view_mask = token_mode ? view_token_mask : nullptr;
   (void)hipGetLastError();
   const hipError_t e = kap::launch_compile_plan(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KAP_ERR_HIP, "compile_plan launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+kap_status kap_compile_plan(int32_t batch, const int32_t *seq_lens, const int32_t *full_block_table,
+                            int32_t fbt_stride, const int32_t *span_offsets, int32_t num_spans,
+                            const int32_t *span_start, const int32_t *span_len,
+                            const float *span_prior, const int32_t *prefix_tokens,
+                            const int32_t *suffix_tokens, const int32_t *budget_tokens,
+                            kap_select_policy policy, int64_t num_pages, int32_t view_capacity,
+                            int32_t *view_block_table, int32_t *view_logical_block,
+                            int32_t *view_num_blocks, int32_t *view_tokens, int32_t *spans_taken,
+                            int32_t *plan_status, int32_t *span_selected, void *workspace,
+                            size_t workspace_bytes, void *stream) {
+  return compile_plan(batch, seq_lens, full_block_table, fbt_stride, span_offsets, num_spans,
+                      span_start, span_len, span_prior, prefix_tokens, suffix_tokens,
+                      budget_tokens, policy, num_pages, view_capacity, view_block_table,
+                      view_logical_block, nullptr, false, view_num_blocks, view_tokens,
+                      spans_taken, plan_status, span_selected, workspace, workspace_bytes,
+                      stream);
+}
+
+kap_status kap_compile_plan_masked(int32_t batch, const int32_t *seq_lens,
+                                   const int32_t *full_block_table, int32_t fbt_stride,
+                                   const int32_t *span_offsets, int32_t num_spans,
+                                   const int32_t *span_start, const int32_t *span_len,
+                                   const float *span_prior, const int32_t *prefix_tokens,
+                                   const int32_t *suffix_tokens, const int32_t *budget_tokens,
+                                   kap_select_policy policy, int64_t num_pages,
+                                   int32_t view_capacity, int32_t *view_block_table,
+                                   int32_t *view_logical_block, uint32_t *view_token_mask,
+                                   int32_t *view_num_blocks, int32_t *view_tokens,
+                                   int32_t *spans_taken, int32_t *plan_status,
+                                   int32_t *span_selected, void *workspace,
+                                   size_t workspace_bytes, void *stream) {
+  return compile_plan(batch, seq_lens, full_block_table, fbt_stride, span_offsets, num_spans,
+                      span_start, span_len, span_prior, prefix_tokens, suffix_tokens,
+                      budget_tokens, policy, num_pages, view_capacity, view_block_table,
+                      view_logical_block, view_token_mask, true, view_num_blocks, view_tokens,
+                      spans_taken, plan_status, span_selected, workspace, workspace_bytes,
+                      stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -365,12 +411,14 @@ size_t kap_selected_decode_workspace_bytes(const kap_kv_cache *kv, int32_t batch
   return partial_bytes(kv, batch, 1, p);
 }
 
-kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void *q,
-                               const int32_t *seq_lens, const int32_t *view_block_table,
-                               const int32_t *view_logical_block, int32_t view_stride,
-                               const int32_t *view_num_blocks, int32_t max_view_blocks,
-                               float sm_scale, int32_t num_splits, float *out, float *lse,
-                               void *workspace, size_t workspace_bytes, void *stream) {
+static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                  const int32_t *seq_lens, const int32_t *view_block_table,
+                                  const int32_t *view_logical_block,
+                                  const uint32_t *view_token_mask, bool masked,
+                                  int32_t view_stride, const int32_t *view_num_blocks,
+                                  int32_t max_view_blocks, float sm_scale, int32_t num_splits,
+                                  float *out, float *lse, void *workspace,
+                                  size_t workspace_bytes, void *stream) {
   kap_status st = check_kv(kv);
   if (st != KAP_OK) return st;
   if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
@@ -388,6 +436,8 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
     return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
   if (max_view_blocks > 0 && (!view_block_table || !view_logical_block))
     return fail(KAP_ERR_INVALID_ARGUMENT, "view tables are NULL");
+  if (masked && max_view_blocks > 0 && !view_token_mask)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "view_token_mask is NULL");
   if (!aligned(q, 16) || !aligned(out, 16))
     return fail(KAP_ERR_INVALID_ARGUMENT, "q and out must be 16-byte aligned");
   const SplitPlan p = plan_decode(kv, batch, max_view_blocks, num_splits);
@@ -419,6 +469,8 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
   a.block_table = no_table ? seq_lens : view_block_table;
   a.bt_stride = no_table ? 0 : view_stride;
   a.logical_block = no_table ? seq_lens : view_logical_block;
+  if (masked)
+    a.token_mask = no_table ? reinterpret_cast<const uint32_t *>(seq_lens) : view_token_mask;
   a.num_blocks = view_num_blocks;
   a.max_blocks = max_view_blocks;
   a.causal = 0;
@@ -426,6 +478,29 @@ kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void
   a.out = out;
   a.lse = lse;
   return launch_attention(a, kv, p, true, workspace, static_cast<hipStream_t>(stream));
+}
+
+kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void *q,
+                               const int32_t *seq_lens, const int32_t *view_block_table,
+                               const int32_t *view_logical_block, int32_t view_stride,
+                               const int32_t *view_num_blocks, int32_t max_view_blocks,
+                               float sm_scale, int32_t num_splits, float *out, float *lse,
+                               void *workspace, size_t workspace_bytes, void *stream) {
+  return selected_decode(kv, batch, q, seq_lens, view_block_table, view_logical_block, nullptr,
+                         false, view_stride, view_num_blocks, max_view_blocks, sm_scale,
+                         num_splits, out, lse, workspace, workspace_bytes, stream);
+}
+
+kap_status kap_selected_decode_masked(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                      const int32_t *seq_lens, const int32_t *view_block_table,
+                                      const int32_t *view_logical_block,
+                                      const uint32_t *view_token_mask, int32_t view_stride,
+                                      const int32_t *view_num_blocks, int32_t max_view_blocks,
+                                      float sm_scale, int32_t num_splits, float *out, float *lse,
+                                      void *workspace, size_t workspace_bytes, void *stream) {
+  return selected_decode(kv, batch, q, seq_lens, view_block_table, view_logical_block,
+                         view_token_mask, true, view_stride, view_num_blocks, max_view_blocks,
+                         sm_scale, num_splits, out, lse, workspace, workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------

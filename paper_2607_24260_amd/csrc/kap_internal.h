@@ -13,6 +13,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kPlanThreads = 256;
 constexpr int kGenericPagesPerSplit = 64;   // 1024 keys staged per generic work item
 constexpr int kMaxPlanPages = 262144;       // pages per sequence the plan bitmap covers
+constexpr int kMaxTokenPlanPages = 16384;   // the same with a bit per token (32 KB of LDS)
 
 enum KvType { kF32 = 0, kBF16 = 1, kFP8 = 2 };
 
@@ -41,6 +42,8 @@ struct PlanArgs {
   int32_t *status;
   int32_t *span_selected;
   int32_t *perm;  // workspace: [num_spans] rank -> local span index
+  int token_mode = 0;             // 1: a bit per token (the plan also writes view_mask)
+  uint32_t *view_mask = nullptr;  // token mode: [batch][capacity] 16-bit token masks
 };
 
 // One attention call (decode or verify) after host validation.
@@ -78,6 +81,9 @@ struct AttnArgs {
   float *part_o;    // normalised partial outputs
   float *part_lse;  // log2-domain partial LSE
   int32_t *tickets; // [batch][Hkv] arrival counters of the fused merge (zero between calls)
+  // decode over a token-granular view: [batch][bt_stride] masks, bit t = token
+  // t of the view page is visible; NULL: every token below seq_len is
+  const uint32_t *token_mask = nullptr;
   float *out;       // [batch * R][D]
   float *lse;       // [batch * R]
 };

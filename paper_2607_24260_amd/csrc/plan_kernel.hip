@@ -3,16 +3,18 @@
 //
 // Per sequence the workgroup
 //   1. checks the CSR bounds, the length and the scores (status codes),
-//   2. marks the mandatory prefix / suffix pages in an LDS page bitmap,
+//   2. marks the mandatory prefix / suffix in an LDS bitmap,
 //   3. ranks the spans by (prior desc, start asc, index asc) -- every thread
 //      counts, for its spans, how many spans precede them, and writes the
 //      inverse permutation to the workspace,
 //   4. walks the spans in rank order with one wavefront: the 64 lanes test the
-//      span's pages against the bitmap, a wavefront ballot counts the new
-//      pages (their cost in visible tokens), and the span is taken when it fits
-//      the budget,
+//      span against the bitmap, a wavefront reduction counts what is new (its
+//      cost in visible tokens), and the span is taken when it fits the budget,
 //   5. compacts the bitmap into the ascending logical-page list and maps it
 //      through the full block table.
+// Page mode keeps one bit per page; token mode (the visibility mask of
+// Sec. 3.1 at token resolution) one bit per token, and also emits each view
+// page's 16-bit mask of visible tokens.
 // Selection uses integer arithmetic only (float priors are only compared), so
 // the plan is bit-for-bit deterministic.
 #include "kap_internal.h"
@@ -52,8 +54,24 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *s_tmp, int *tota
   return before + x - v;
 }
 
+// Bits of token word w (tokens 32w .. 32w + 31) that lie in [x, e).
+__device__ __forceinline__ uint32_t range_bits(int w, int x, int e) {
+  const int lo = min(max(x - 32 * w, 0), 32);
+  const int hi = min(max(e - 32 * w, 0), 32);
+  return (uint32_t)(((1ull << hi) - 1ull) ^ ((1ull << lo) - 1ull));
+}
+
+// Sum over the wavefront of a per-lane count in [0, 63]: one ballot per bit.
+__device__ __forceinline__ int wave_count_sum(int c) {
+  int s = 0;
+#pragma unroll
+  for (int k = 0; k < 6; ++k) s += __popcll(__ballot((c >> k) & 1)) << k;
+  return s;
+}
+
+template <bool TOK>
 __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) {
-  extern __shared__ uint32_t bitmap[];
+  extern __shared__ uint32_t bitmap[];   // page mode: bit per page; token mode: bit per token
   __shared__ int s_flag;
   __shared__ int s_scan[kPlanThreads / 64];
   __shared__ long long s_used;
@@ -102,17 +120,23 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     return;
   }
 
-  // -- mandatory pages --------------------------------------------------------
-  const int W = (NP + 31) / 32;
-  for (int w = tid; w < W; w += kPlanThreads) bitmap[w] = 0u;
-  __syncthreads();
+  // -- mandatory prefix / suffix ----------------------------------------------
   const int pre = min(max(a.prefix[b], 0), L);
   const int suf_start = max(0, L - max(a.suffix[b], 1));
-  const int pre_pages = (pre + kPage - 1) / kPage;     // pages [0, pre_pages)
-  const int suf_page0 = suf_start / kPage;             // pages [suf_page0, NP)
-  for (int p = tid; p < pre_pages; p += kPlanThreads) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
-  for (int p = suf_page0 + tid; p < NP; p += kPlanThreads)
-    atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+  const int W = TOK ? (L + 31) / 32 : (NP + 31) / 32;  // bitmap words
+  if constexpr (TOK) {
+    // tokens [0, pre) and [suf_start, L); no bit at or past L is ever set
+    for (int w = tid; w < W; w += kPlanThreads)
+      bitmap[w] = range_bits(w, 0, pre) | range_bits(w, suf_start, L);
+  } else {
+    for (int w = tid; w < W; w += kPlanThreads) bitmap[w] = 0u;
+    __syncthreads();
+    const int pre_pages = (pre + kPage - 1) / kPage;     // pages [0, pre_pages)
+    const int suf_page0 = suf_start / kPage;             // pages [suf_page0, NP)
+    for (int p = tid; p < pre_pages; p += kPlanThreads) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+    for (int p = suf_page0 + tid; p < NP; p += kPlanThreads)
+      atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+  }
 
   // -- rank the spans ---------------------------------------------------------
   // rank(i) = number of spans ordered before span i; keys are staged through
@@ -142,16 +166,20 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   }
   __syncthreads();
 
-  // -- visible tokens of the mandatory pages ---------------------------------
-  const int last_valid = L - kPage * (NP - 1);          // 1..16
+  // -- visible tokens of the mandatory part -----------------------------------
   {
     int c = 0;
     for (int w = tid; w < W; w += kPlanThreads) c += __popc(bitmap[w]);
     int total = 0;
     block_exclusive_scan(c, s_scan, &total);
     if (tid == 0) {
-      // the last page is always selected (suffix >= 1 token)
-      s_used = (long long)kPage * total - (kPage - last_valid);
+      if constexpr (TOK) {
+        s_used = total;
+      } else {
+        // the last page is always selected (suffix >= 1 token)
+        const int last_valid = L - kPage * (NP - 1);    // 1..16
+        s_used = (long long)kPage * total - (kPage - last_valid);
+      }
       s_taken = 0;
     }
   }
@@ -159,9 +187,10 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
 
   // -- greedy selection in rank order (one wavefront) -------------------------
   // Lane l holds the clipped span of rank r0 + l, so one global round trip
-  // serves 64 decisions. Every page except the last (always selected) holds 16
-  // tokens, so a span's cost is 16 x (its pages not yet selected), counted with
-  // a wavefront ballot over 64 pages at a time.
+  // serves 64 decisions. Page mode: every page except the last (always
+  // selected) holds 16 tokens, so a span costs 16 x (its pages not yet
+  // selected), counted with a ballot over 64 pages at a time. Token mode: a
+  // span costs its tokens not yet visible, 64 bitmap words at a time.
   if (tid < 64) {
     long long used = s_used;
     int taken = 0;
@@ -184,17 +213,32 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
         const int x = __builtin_amdgcn_readlane(my_x, j);
         const int e = __builtin_amdgcn_readlane(my_e, j);
         if (e <= x) continue;                           // ignored
-        const int p0 = x / kPage;
-        const int p1 = (e + kPage - 1) / kPage;
-        int new_pages = 0;
-        for (int p = p0; p < p1; p += 64) {
-          const int pp = p + lane;
-          const bool fresh = pp < p1 && !((bitmap[pp >> 5] >> (pp & 31)) & 1u);
-          new_pages += __popcll(__ballot(fresh));
+        long long cost = 0;
+        int u0, u1;                                     // bitmap units (pages / words) touched
+        if constexpr (TOK) {
+          u0 = x >> 5;
+          u1 = ((e - 1) >> 5) + 1;
+          for (int w = u0 + lane; w - lane < u1; w += 64) {
+            const int c = w < u1 ? __popc(range_bits(w, x, e) & ~bitmap[w]) : 0;
+            cost += wave_count_sum(c);
+          }
+        } else {
+          u0 = x / kPage;
+          u1 = (e + kPage - 1) / kPage;
+          int new_pages = 0;
+          for (int p = u0; p < u1; p += 64) {
+            const int pp = p + lane;
+            const bool fresh = pp < u1 && !((bitmap[pp >> 5] >> (pp & 31)) & 1u);
+            new_pages += __popcll(__ballot(fresh));
+          }
+          cost = (long long)kPage * new_pages;
         }
-        const long long cost = (long long)kPage * new_pages;
         if (used + cost <= T) {
-          for (int p = p0 + lane; p < p1; p += 64) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+          if constexpr (TOK) {
+            for (int w = u0 + lane; w < u1; w += 64) bitmap[w] |= range_bits(w, x, e);
+          } else {
+            for (int p = u0 + lane; p < u1; p += 64) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
+          }
           used += cost;
           ++taken;
           if (lane == 0 && a.span_selected) a.span_selected[i] = 1;
@@ -213,11 +257,16 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __syncthreads();
 
   // -- compaction: ascending logical pages -> block table ---------------------
+  // Token mode: page p is the half p & 1 of token word p >> 1 and is in the
+  // view when any of its 16 bits is set; that half is its token mask.
   const int chunk = (W + kPlanThreads - 1) / kPlanThreads;
   const int w0 = min(W, tid * chunk);
   const int w1 = min(W, w0 + chunk);
   int mine = 0;
-  for (int w = w0; w < w1; ++w) mine += __popc(bitmap[w]);
+  for (int w = w0; w < w1; ++w) {
+    const uint32_t x = bitmap[w];
+    mine += TOK ? ((x & 0xFFFFu) != 0u) + ((x >> 16) != 0u) : __popc(x);
+  }
   if (tid == 0) s_flag = 0;
   int nblk = 0;
   const int first = block_exclusive_scan(mine, s_scan, &nblk);
@@ -230,17 +279,26 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   int32_t *vbt = a.view_bt + (size_t)b * a.capacity;
   int32_t *vlb = a.view_lblk + (size_t)b * a.capacity;
   bool bad = false;
+  auto emit = [&](int p, uint32_t mask) {
+    const int page = fbt_row[p];
+    bad |= (page < 0) || ((int64_t)page >= a.num_pages);
+    vlb[out] = p;
+    vbt[out] = page;
+    if constexpr (TOK) a.view_mask[(size_t)b * a.capacity + out] = mask;
+    ++out;
+  };
   for (int w = w0; w < w1; ++w) {
-    uint32_t bits = bitmap[w];
-    while (bits) {
-      const int bit = __ffs(bits) - 1;
-      bits &= bits - 1u;
-      const int p = w * 32 + bit;
-      const int page = fbt_row[p];
-      bad |= (page < 0) || ((int64_t)page >= a.num_pages);
-      vlb[out] = p;
-      vbt[out] = page;
-      ++out;
+    const uint32_t x = bitmap[w];
+    if constexpr (TOK) {
+      if (x & 0xFFFFu) emit(2 * w, x & 0xFFFFu);
+      if (x >> 16) emit(2 * w + 1, x >> 16);
+    } else {
+      uint32_t bits = x;
+      while (bits) {
+        const int bit = __ffs(bits) - 1;
+        bits &= bits - 1u;
+        emit(w * 32 + bit, 0u);
+      }
     }
   }
   if (bad) s_flag = 1;
@@ -257,12 +315,22 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   }
 }
 
+size_t plan_lds_bytes(int fbt_stride, bool token_mode) {
+  // page mode: a bit per page; token mode: a bit per token (16 per page)
+  const size_t words = token_mode ? ((size_t)fbt_stride * kPage + 31) / 32
+                                  : ((size_t)fbt_stride + 31) / 32;
+  return (words + 1) * sizeof(uint32_t);   // + a spare word
+}
+
 }  // namespace
 
 hipError_t launch_compile_plan(const PlanArgs &a, hipStream_t s) {
-  const size_t words = (size_t)(a.fbt_stride + 31) / 32 + 1;   // + spare count word
-  hipLaunchKernelGGL(compile_plan_kernel, dim3(a.batch), dim3(kPlanThreads),
-                     words * sizeof(uint32_t), s, a);
+  const bool tok = a.token_mode != 0;
+  const size_t lds = plan_lds_bytes(a.fbt_stride, tok);
+  if (tok)
+    hipLaunchKernelGGL(compile_plan_kernel<true>, dim3(a.batch), dim3(kPlanThreads), lds, s, a);
+  else
+    hipLaunchKernelGGL(compile_plan_kernel<false>, dim3(a.batch), dim3(kPlanThreads), lds, s, a);
   return hipGetLastError();
 }
 

@@ -41,8 +41,8 @@ KAP_PLAN_BAD_SPANS = 5
 PAGE = 16
 
 EXPORTS = (
-    "kap_compile_plan", "kap_compile_plan_workspace_bytes",
-    "kap_selected_decode", "kap_selected_decode_workspace_bytes",
+    "kap_compile_plan", "kap_compile_plan_workspace_bytes", "kap_compile_plan_masked",
+    "kap_selected_decode", "kap_selected_decode_workspace_bytes", "kap_selected_decode_masked",
     "kap_verify", "kap_verify_workspace_bytes",
     "kap_append_kv", "kap_compact_view", "kap_fallback_update",
     "kap_accept_top3", "kap_accept_top3_workspace_bytes",
@@ -92,11 +92,19 @@ def load_library(path: str = LIB_PATH):
     lib.kap_compile_plan.argtypes = [
         _I32, _P, _P, _I32, _P, _I32, _P, _P, _P, _P, _P, _P, _I32, _I64, _I32,
         _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.kap_compile_plan_masked.restype = _I32
+    lib.kap_compile_plan_masked.argtypes = [
+        _I32, _P, _P, _I32, _P, _I32, _P, _P, _P, _P, _P, _P, _I32, _I64, _I32,
+        _P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]
     lib.kap_compile_plan_workspace_bytes.restype = _SZ
     lib.kap_compile_plan_workspace_bytes.argtypes = [_I32, _I32, _I32]
     lib.kap_selected_decode.restype = _I32
     lib.kap_selected_decode.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _I32, _P, _I32, _F, _I32,
+        _P, _P, _P, _SZ, _P]
+    lib.kap_selected_decode_masked.restype = _I32
+    lib.kap_selected_decode_masked.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _P, _I32, _P, _I32, _F, _I32,
         _P, _P, _P, _SZ, _P]
     lib.kap_selected_decode_workspace_bytes.restype = _SZ
     lib.kap_selected_decode_workspace_bytes.argtypes = [
@@ -363,13 +371,11 @@ def compile_plan_workspace_bytes(batch: int, num_spans: int, fbt_stride: int) ->
     return int(load_library().kap_compile_plan_workspace_bytes(batch, num_spans, fbt_stride))
 
 
-def compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
-                 prefix_tokens, suffix_tokens, budget_tokens, *, num_pages: int,
-                 view_capacity: int, policy: int = KAP_SELECT_SKIP, out: Optional[dict] = None,
-                 workspace: Optional[torch.Tensor] = None, stream=None) -> dict:
-    """Runtime access plan of every sequence (Alg. 1). Returns a dict of GPU
-    tensors: view_block_table, view_logical_block [B][view_capacity],
-    view_num_blocks, view_tokens, spans_taken, plan_status [B], span_selected [S]."""
+def _plan_call(seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
+               prefix_tokens, suffix_tokens, budget_tokens, num_pages, view_capacity, policy,
+               out, workspace, token_granular, stream):
+    """Validate and marshal one kap_compile_plan[_masked] call: returns
+    (function, ctypes arguments, out)."""
     lib = load_library()
     i32 = torch.int32
     _dev(seq_lens, "seq_lens", i32, 1)
@@ -403,21 +409,48 @@ def compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len,
             "plan_status": torch.empty(B, dtype=i32, device=dev),
             "span_selected": torch.empty(S, dtype=i32, device=dev),
         }
-    for name in ("view_block_table", "view_logical_block"):
+        if token_granular:
+            out["view_token_mask"] = torch.empty((B, cap), dtype=i32, device=dev)
+    tables = ("view_block_table", "view_logical_block") + (
+        ("view_token_mask",) if token_granular else ())
+    for name in tables:
+        if name not in out:
+            raise ValueError(f"out needs {name}")
         _dev(out[name], name, i32, 2)
         if out[name].shape != (B, view_capacity):
             raise ValueError(f"{name} must be [batch][view_capacity]")
     need = compile_plan_workspace_bytes(B, S, full_block_table.shape[1])
     workspace, have = _workspace(need, dev, workspace)
-    st = lib.kap_compile_plan(
-        B, _ptr(seq_lens), _ptr(full_block_table), full_block_table.shape[1], _ptr(span_offsets),
-        S, _ptr(span_start), _ptr(span_len), _ptr(span_prior), _ptr(prefix_tokens),
-        _ptr(suffix_tokens), _ptr(budget_tokens), int(policy), int(num_pages), int(view_capacity),
-        _ptr(out["view_block_table"]), _ptr(out["view_logical_block"]),
-        _ptr(out["view_num_blocks"]), _ptr(out["view_tokens"]), _ptr(out["spans_taken"]),
-        _ptr(out["plan_status"]), _ptr(out.get("span_selected")), _ptr(workspace), have,
-        _stream(stream))
-    _check(st)
+    head = (B, _ptr(seq_lens), _ptr(full_block_table), full_block_table.shape[1],
+            _ptr(span_offsets), S, _ptr(span_start), _ptr(span_len), _ptr(span_prior),
+            _ptr(prefix_tokens), _ptr(suffix_tokens), _ptr(budget_tokens), int(policy),
+            int(num_pages), int(view_capacity), _ptr(out["view_block_table"]),
+            _ptr(out["view_logical_block"]))
+    mask = (_ptr(out["view_token_mask"]),) if token_granular else ()
+    tail = (_ptr(out["view_num_blocks"]), _ptr(out["view_tokens"]), _ptr(out["spans_taken"]),
+            _ptr(out["plan_status"]), _ptr(out.get("span_selected")), _ptr(workspace), have,
+            _stream(stream))
+    fn = lib.kap_compile_plan_masked if token_granular else lib.kap_compile_plan
+    keep = (seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
+            prefix_tokens, suffix_tokens, budget_tokens, out, workspace)
+    return fn, head + mask + tail, out, keep
+
+
+def compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
+                 prefix_tokens, suffix_tokens, budget_tokens, *, num_pages: int,
+                 view_capacity: int, policy: int = KAP_SELECT_SKIP, out: Optional[dict] = None,
+                 workspace: Optional[torch.Tensor] = None, token_granular: bool = False,
+                 stream=None) -> dict:
+    """Runtime access plan of every sequence (Alg. 1). Returns a dict of GPU
+    tensors: view_block_table, view_logical_block [B][view_capacity],
+    view_num_blocks, view_tokens, spans_taken, plan_status [B], span_selected [S];
+    with ``token_granular`` (kap_compile_plan_masked) also view_token_mask
+    [B][view_capacity] (int32 holding the 16-bit masks)."""
+    fn, args, out, _ = _plan_call(seq_lens, full_block_table, span_offsets, span_start,
+                                  span_len, span_prior, prefix_tokens, suffix_tokens,
+                                  budget_tokens, num_pages, view_capacity, policy, out,
+                                  workspace, token_granular, stream)
+    _check(fn(*args))
     return out
 
 
@@ -449,11 +482,10 @@ def _outputs(shape, dev, out, lse):
     return out, lse
 
 
-def selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
-                    view_num_blocks, max_view_blocks: int, sm_scale: float, *,
-                    num_splits: int = 0, out=None, lse=None, workspace=None, stream=None):
-    """One proposal step over the selected-KV view. q [B][Hq][D]; returns
-    (out [B][Hq][D] float32, lse [B][Hq] float32)."""
+def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
+                 view_num_blocks, max_view_blocks, sm_scale, num_splits, out, lse, workspace,
+                 view_token_mask, stream):
+    """Validate and marshal one kap_selected_decode[_masked] call."""
     lib = load_library()
     _dev(q, "q", kv.q_dtype, 3)
     B = q.shape[0]
@@ -465,18 +497,40 @@ def selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_blo
     _dev(view_logical_block, "view_logical_block", torch.int32, 2)
     if view_block_table.shape != view_logical_block.shape or view_block_table.shape[0] != B:
         raise ValueError("view tables must both be [batch][view_stride]")
+    if view_token_mask is not None:
+        _dev(view_token_mask, "view_token_mask", torch.int32, 2)
+        if view_token_mask.shape != view_block_table.shape:
+            raise ValueError("view_token_mask must be shaped like the view tables")
     if seq_lens.shape[0] != B or view_num_blocks.shape[0] != B:
         raise ValueError("seq_lens / view_num_blocks must have batch entries")
     out, lse = _outputs((B, kv.num_q_heads, kv.head_dim), q.device, out, lse)
     need = selected_decode_workspace_bytes(kv, B, max_view_blocks, num_splits)
     workspace, have = _workspace(need, q.device, workspace)
-    st = lib.kap_selected_decode(
-        ctypes.byref(kv.struct), B, _ptr(q), _ptr(seq_lens), _ptr(view_block_table),
-        _ptr(view_logical_block), view_block_table.shape[1], _ptr(view_num_blocks),
-        int(max_view_blocks), float(sm_scale), int(num_splits), _ptr(out), _ptr(lse),
-        _ptr(workspace), have, _stream(stream))
-    _check(st)
-    return out, lse
+    head = (ctypes.byref(kv.struct), B, _ptr(q), _ptr(seq_lens), _ptr(view_block_table),
+            _ptr(view_logical_block))
+    mask = () if view_token_mask is None else (_ptr(view_token_mask),)
+    tail = (view_block_table.shape[1], _ptr(view_num_blocks), int(max_view_blocks),
+            float(sm_scale), int(num_splits), _ptr(out), _ptr(lse), _ptr(workspace), have,
+            _stream(stream))
+    fn = lib.kap_selected_decode if view_token_mask is None else lib.kap_selected_decode_masked
+    keep = (kv, q, seq_lens, view_block_table, view_logical_block, view_num_blocks,
+            view_token_mask, out, lse, workspace)
+    return fn, head + mask + tail, (out, lse), keep
+
+
+def selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
+                    view_num_blocks, max_view_blocks: int, sm_scale: float, *,
+                    num_splits: int = 0, out=None, lse=None, workspace=None,
+                    view_token_mask=None, stream=None):
+    """One proposal step over the selected-KV view. q [B][Hq][D]; returns
+    (out [B][Hq][D] float32, lse [B][Hq] float32). ``view_token_mask``
+    [B][view_stride] (a token-granular plan's masks) calls
+    kap_selected_decode_masked."""
+    fn, args, res, _ = _decode_call(kv, q, seq_lens, view_block_table, view_logical_block,
+                                    view_num_blocks, max_view_blocks, sm_scale, num_splits,
+                                    out, lse, workspace, view_token_mask, stream)
+    _check(fn(*args))
+    return res
 
 
 def verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scale: float, *,
@@ -527,22 +581,17 @@ class BoundCall:
 
 def bind_selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
                          view_num_blocks, max_view_blocks: int, sm_scale: float, out, lse,
-                         workspace=None, num_splits: int = 0, stream=None) -> BoundCall:
-    lib = load_library()
-    selected_decode(kv, q, seq_lens, view_block_table, view_logical_block, view_num_blocks,
-                    max_view_blocks, sm_scale, num_splits=num_splits, out=out, lse=lse,
-                    workspace=workspace, stream=stream)          # validates once
+                         workspace=None, num_splits: int = 0, view_token_mask=None,
+                         stream=None) -> BoundCall:
     need = selected_decode_workspace_bytes(kv, q.shape[0], max_view_blocks, num_splits)
     have = 0 if workspace is None else workspace.numel() * workspace.element_size()
     if need > have:
         raise ValueError(f"workspace of {need} bytes required")
-    args = (ctypes.byref(kv.struct), q.shape[0], _ptr(q), _ptr(seq_lens),
-            _ptr(view_block_table), _ptr(view_logical_block), view_block_table.shape[1],
-            _ptr(view_num_blocks), int(max_view_blocks), float(sm_scale), int(num_splits),
-            _ptr(out), _ptr(lse), _ptr(workspace), have, _stream(stream))
-    return BoundCall(lib.kap_selected_decode, args,
-                     (kv, q, seq_lens, view_block_table, view_logical_block, view_num_blocks,
-                      out, lse, workspace))
+    fn, args, _, keep = _decode_call(kv, q, seq_lens, view_block_table, view_logical_block,
+                                     view_num_blocks, max_view_blocks, sm_scale, num_splits,
+                                     out, lse, workspace, view_token_mask, stream)
+    _check(fn(*args))                                             # validates once
+    return BoundCall(fn, args, keep)
 
 
 def bind_verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scale: float,
@@ -565,24 +614,16 @@ def bind_verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm
 def bind_compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len,
                       span_prior, prefix_tokens, suffix_tokens, budget_tokens, *, num_pages: int,
                       view_capacity: int, out: dict, workspace=None,
-                      policy: int = KAP_SELECT_SKIP, stream=None) -> BoundCall:
-    lib = load_library()
-    compile_plan(seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
-                 prefix_tokens, suffix_tokens, budget_tokens, num_pages=num_pages,
-                 view_capacity=view_capacity, policy=policy, out=out, workspace=workspace,
-                 stream=stream)
+                      policy: int = KAP_SELECT_SKIP, token_granular: bool = False,
+                      stream=None) -> BoundCall:
     B, S = seq_lens.shape[0], span_start.shape[0]
     need = compile_plan_workspace_bytes(B, S, full_block_table.shape[1])
     have = 0 if workspace is None else workspace.numel() * workspace.element_size()
     if need > have:
         raise ValueError(f"workspace of {need} bytes required")
-    args = (B, _ptr(seq_lens), _ptr(full_block_table), full_block_table.shape[1],
-            _ptr(span_offsets), S, _ptr(span_start), _ptr(span_len), _ptr(span_prior),
-            _ptr(prefix_tokens), _ptr(suffix_tokens), _ptr(budget_tokens), int(policy),
-            int(num_pages), int(view_capacity), _ptr(out["view_block_table"]),
-            _ptr(out["view_logical_block"]), _ptr(out["view_num_blocks"]),
-            _ptr(out["view_tokens"]), _ptr(out["spans_taken"]), _ptr(out["plan_status"]),
-            _ptr(out.get("span_selected")), _ptr(workspace), have, _stream(stream))
-    return BoundCall(lib.kap_compile_plan, args,
-                     (seq_lens, full_block_table, span_offsets, span_start, span_len, span_prior,
-                      prefix_tokens, suffix_tokens, budget_tokens, out, workspace))
+    fn, args, out, keep = _plan_call(seq_lens, full_block_table, span_offsets, span_start,
+                                     span_len, span_prior, prefix_tokens, suffix_tokens,
+                                     budget_tokens, num_pages, view_capacity, policy, out,
+                                     workspace, token_granular, stream)
+    _check(fn(*args))                                             # validates once
+    return BoundCall(fn, args, keep)

@@ -136,6 +136,28 @@ def test_compile_plan_rejects_bad_arguments(lib):
     assert lib.kap_compile_plan_workspace_bytes(1, 0, 8) == 0
 
 
+def masked_plan_call(lib, fbt_stride=8, cap=8, mask=FAKE, ws=FAKE, ws_bytes=256):
+    return lib.kap_compile_plan_masked(1, FAKE, FAKE, fbt_stride, FAKE, 4, FAKE, FAKE, FAKE,
+                                       FAKE, FAKE, FAKE, 0, 100, cap, FAKE, FAKE, mask, FAKE,
+                                       FAKE, FAKE, FAKE, None, ws, ws_bytes, None)
+
+
+def test_token_granular_calls_reject_bad_arguments(lib):
+    # the token bitmap covers 16384 pages; the page bitmap 262144
+    assert masked_plan_call(lib, fbt_stride=16385) == K.KAP_ERR_UNSUPPORTED
+    assert plan_call(lib, fbt_stride=16385, ws=None) == K.KAP_ERR_WORKSPACE_TOO_SMALL
+    assert masked_plan_call(lib, mask=None) == K.KAP_ERR_INVALID_ARGUMENT
+    assert b"view_token_mask" in lib.kap_last_error()
+    assert masked_plan_call(lib, ws=None, ws_bytes=0) == K.KAP_ERR_WORKSPACE_TOO_SMALL
+    kv = kv_struct()
+    st = lib.kap_selected_decode_masked(ctypes.byref(kv), 2, FAKE, FAKE, FAKE, FAKE, None, 8,
+                                        FAKE, 8, 1.0, 0, FAKE, FAKE, None, 0, None)
+    assert st == K.KAP_ERR_INVALID_ARGUMENT and b"view_token_mask" in lib.kap_last_error()
+    st = lib.kap_selected_decode_masked(ctypes.byref(kv), 0, FAKE, FAKE, FAKE, FAKE, FAKE, 8,
+                                        FAKE, 8, 1.0, 0, FAKE, FAKE, None, 0, None)
+    assert st == K.KAP_OK
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     with pytest.raises(ValueError, match="GPU tensor"):
