@@ -153,6 +153,14 @@ def cpu_baseline(w, budget_s=12.0):
         if secs >= budget_s:
             break
     aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    model = ""
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {
         "value": round(total / secs / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
         "kind": "oracle",
@@ -161,7 +169,122 @@ def cpu_baseline(w, budget_s=12.0):
                    f"calls over all {w.batch} sequences; fp64 numpy"),
         "seconds": round(secs, 3),
         "host_cpus": os.cpu_count(), "affinity_cpus": aff, "blas_threads": blas_threads,
+        "cpu_model": model,
     }
+
+
+def stream_read_ceiling(torch, K, dev):
+    """kap_stream_read (a plain coalesced read kernel) at the decode call's size
+    (118 MB, 10 rotating buffers) and the verify call's size (2 GiB, 2 buffers):
+    the practical HBM read rate the attention kernels are compared with."""
+    out = {}
+    for name, nbytes, nbuf, n in (("decode_size", 118 << 20, 10, 200), ("verify_size", 2 << 30, 2, 16)):
+        bufs = [torch.ones(nbytes, dtype=torch.uint8, device=dev) for _ in range(nbuf)]
+        sink = torch.zeros(1, dtype=torch.int32, device=dev)
+        t = time_loop(lambda i: K.stream_read(bufs[i % nbuf], sink), n, 5, torch)
+        out[name] = {"bytes": nbytes, "us_per_call": round(t * 1e3, 2),
+                     "gbs": round(nbytes / (t * 1e-3) / 1e9, 1)}
+        del bufs
+    torch.cuda.empty_cache()
+    return out
+
+
+# Context buckets of the paper's Table 2: length, retained ratio s, Top-3 acceptance h
+TAB2 = [(4096, 0.401, 0.958), (8192, 0.344, 0.957), (16384, 0.242, 0.957),
+        (32768, 0.161, 0.956), (65536, 0.108, 0.962), (131072, 0.055, 0.953)]
+
+
+def _attention_calls(torch, K, w, R, dev):
+    """Bound plan, view decode, all-blocks decode and verify calls of workload
+    `w` over R KV replicas; returns the timings (ms) and the plan's s."""
+    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32)).to(dev)
+    B, Hq, D, cap = w.batch, w.num_q_heads, w.head_dim, w.max_pages_per_seq
+    kvs = [K.KVCache(w.k_pages[r], w.v_pages[r], Hq, torch.bfloat16) for r in range(R)]
+    seq_lens, fbt = i32(w.seq_lens), i32(w.full_block_table)
+    plan = K.compile_plan(seq_lens, fbt, i32(w.span_offsets), i32(w.span_start),
+                          i32(w.span_len), torch.as_tensor(w.span_prior).to(dev), i32(w.prefix),
+                          i32(w.suffix), i32(w.budget), num_pages=w.num_pages,
+                          view_capacity=cap)
+    torch.cuda.synchronize()
+    assert np.all(plan["plan_status"].cpu().numpy() == 0)
+    s = plan["view_tokens"].cpu().numpy() / w.seq_lens
+    q_len = w.q_verify[0].shape[1]
+    o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    l = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+    ov = torch.empty((B, q_len, Hq, D), dtype=torch.float32, device=dev)
+    lv = torch.empty((B, q_len, Hq), dtype=torch.float32, device=dev)
+    lblk_f = torch.arange(fbt.shape[1], dtype=torch.int32, device=dev).repeat(B, 1)
+    nb_f = i32(-(-np.asarray(w.seq_lens, dtype=np.int64) // 16))
+    Lmax = int(w.seq_lens.max())
+    ws_d = torch.zeros(max(256, K.selected_decode_workspace_bytes(kvs[0], B, fbt.shape[1])),
+                       dtype=torch.uint8, device=dev)
+    ws_v = torch.zeros(max(256, K.verify_workspace_bytes(kvs[0], B, q_len, Lmax)),
+                       dtype=torch.uint8, device=dev)
+    view = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens, plan["view_block_table"],
+                                   plan["view_logical_block"], plan["view_num_blocks"], cap,
+                                   w.sm_scale, o, l, ws_d) for r in range(R)]
+    full = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens, fbt, lblk_f, nb_f,
+                                   fbt.shape[1], w.sm_scale, o, l, ws_d) for r in range(R)]
+    ver = [K.bind_verify(kvs[r], w.q_verify[0], seq_lens, fbt, Lmax, w.sm_scale, ov, lv, ws_v)
+           for r in range(R)]
+    t_view = time_loop(lambda i: view[i % R](), max(64, 3 * R), 5, torch)
+    t_full = time_loop(lambda i: full[i % R](), max(12, R), 3, torch)
+    t_ver = time_loop(lambda i: ver[i % R](), max(12, R), 3, torch)
+    return t_view, t_full, t_ver, s
+
+
+def rq1_sweep(torch, K, dev):
+    """Kernel-level analog of the paper's Table 2: B = 4 sequences per context
+    bucket with the bucket's retained ratio s as the budget; selected-view
+    decode against all-blocks decode (ideal ratio 1/s), and the attention-only
+    cost ratio of Eq. (6)-(7) with k = 4 and the bucket's h."""
+    from paper_2607_24260_amd import costmodel
+    from paper_2607_24260_amd.workloads import make_workload
+    rows = []
+    for L, s_paper, h in TAB2:
+        kv_bytes = 4 * L * BYTES_PER_TOKEN["bf16"]
+        R = int(min(64, max(2, math.ceil((1 << 30) / (s_paper * kv_bytes)))))
+        w = make_workload(4, device=dev, replicas=R, seq_len=L, n_decode=1, n_verify=1,
+                          budget_frac=s_paper)
+        t_view, t_full, t_ver, s = _attention_calls(torch, K, w, R, dev)
+        rep_ = costmodel.measured(4, h, float(np.mean(s)), t_view, t_full, t_ver)
+        vt = float(np.sum(s * w.seq_lens))
+        rows.append({
+            "seq_len": L, "s_paper": s_paper, "s_plan": round(float(np.mean(s)), 4), "h_paper": h,
+            "decode_view_us": round(t_view * 1e3, 2), "decode_all_blocks_us": round(t_full * 1e3, 2),
+            "verify_us": round(t_ver * 1e3, 2),
+            "access_reduction_measured": round(t_full / t_view, 2),
+            "access_reduction_ideal": round(1.0 / float(np.mean(s)), 2),
+            "decode_view_gbs": round(vt * BYTES_PER_TOKEN["bf16"] / (t_view * 1e-3) / 1e9, 1),
+            "attention_speedup_measured": round(1.0 / rep_.measured_ratio, 3),
+            "attention_speedup_ideal": round(1.0 / rep_.ideal_ratio, 3),
+            "kv_replicas": R})
+        log(f"sweep L={L}: {rows[-1]}")
+        del w
+        torch.cuda.empty_cache()
+    return rows
+
+
+def tp4_share(torch, K, dev):
+    """One GPU's share of the 128K workload under a 4-way head split (the
+    paper's TP = 4): 8 query heads over 2 KV heads of every page."""
+    from paper_2607_24260_amd.workloads import make_workload
+    R = 36
+    w = make_workload(4, device=dev, replicas=R, n_decode=1, n_verify=1, num_q_heads=8,
+                      num_kv_heads=2)
+    t_view, t_full, t_ver, s = _attention_calls(torch, K, w, R, dev)
+    per_tok = 2 * 2 * 128 * 2
+    dec_b = float(np.sum(s * w.seq_lens)) * per_tok
+    ver_b = float(np.sum(w.seq_lens)) * per_tok
+    out = {"heads": "8 query / 2 KV heads (1/4 of 32 / 8)", "kv_replicas": R,
+           "decode_us_per_call": round(t_view * 1e3, 2),
+           "decode_gbs": round(dec_b / (t_view * 1e-3) / 1e9, 1),
+           "verify_us_per_call": round(t_ver * 1e3, 2),
+           "verify_gbs": round(ver_b / (t_ver * 1e-3) / 1e9, 1),
+           "all_blocks_decode_us": round(t_full * 1e3, 2)}
+    del w
+    torch.cuda.empty_cache()
+    return out
 
 
 def ragged_stream(torch, K, dev, reps=3):
@@ -294,6 +417,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-ragged", action="store_true",
                     help="skip the ragged fp8 stream measurement")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the stream-read ceiling, the context sweep and the TP-share run")
     ap.add_argument("--profile", action="store_true",
                     help="only the timed steps (for rocprofv3 runs)")
     ap.add_argument("--calibrate", action="store_true",
@@ -512,6 +637,49 @@ def main():
         log(f"accept_top3: {accept}")
         del lg
 
+    # token-granular visibility (Sec. 3.1 mask at token resolution): the same
+    # spans and budgets, plan in token mode, decode with per-page token masks
+    tokmode = None
+    if cfg == 4:
+        plan_tok = {k: torch.zeros_like(v) for k, v in plan_out.items()}
+        plan_tok["view_token_mask"] = torch.zeros((B, cap), dtype=torch.int32, device=dev)
+        plan_tok_call = K.bind_compile_plan(*plan_in, num_pages=w.num_pages, view_capacity=cap,
+                                            out=plan_tok, workspace=ws_plan, token_granular=True)
+        torch.cuda.synchronize()
+        assert np.all(plan_tok["plan_status"].cpu().numpy() == 0)
+        vt_tok = plan_tok["view_tokens"].cpu().numpy()
+        vb_tok = plan_tok["view_num_blocks"].cpu().numpy()
+        o_t = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        l_t = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        dec_t = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens,
+                                        plan_tok["view_block_table"],
+                                        plan_tok["view_logical_block"],
+                                        plan_tok["view_num_blocks"], cap, w.sm_scale, o_t, l_t,
+                                        ws_dec, view_token_mask=plan_tok["view_token_mask"])
+                 for r in range(R)]
+        t_dec_t = time_loop(lambda i: dec_t[i % R](), 256, 5, torch)
+        t_plan_t = time_loop(lambda i: plan_tok_call(), 50, 3, torch)
+        read_b = int(np.sum(vb_tok)) * 16 * BYTES_PER_TOKEN[w.kv_dtype]
+        tokmode = {
+            "plan_us_per_call": round(t_plan_t * 1e3, 2),
+            "decode_us_per_call": round(t_dec_t * 1e3, 3),
+            "visible_tokens": int(np.sum(vt_tok)),
+            "view_pages": int(np.sum(vb_tok)),
+            "retained_ratio_s_mean": round(float(np.mean(vt_tok / w.seq_lens)), 5),
+            "page_mode_visible_tokens": int(np.sum(view_tokens)),
+            "page_mode_view_pages": int(np.sum(view_blocks)),
+            "decode_page_read_gbs": round(read_b / (t_dec_t * 1e-3) / 1e9, 1),
+        }
+        log(f"token-granular: {tokmode}")
+
+    ceiling = sweep = share = None
+    if cfg == 4 and not args.no_sweep:
+        ceiling = stream_read_ceiling(torch, K, dev)
+        log(f"stream-read ceiling: {ceiling}")
+        sweep = rq1_sweep(torch, K, dev)
+        share = tp4_share(torch, K, dev)
+        log(f"tp4 share: {share}")
+
     ragged = None
     if not args.no_ragged and cfg == 4:
         ragged = ragged_stream(torch, K, dev)
@@ -546,6 +714,7 @@ def main():
         },
         "pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "decode_steps_per_s": round(1e3 / t_dec, 1),
+        "decode_tokens_per_s": round(B * 1e3 / t_dec, 1),
         "decode_us_per_call": round(t_dec * 1e3, 3),
         "decode_effective_gbs": round(dec_gbs, 1),
         "decode_pct_hbm_peak": round(100 * dec_gbs / HBM_PEAK_GBS, 2),
@@ -567,6 +736,10 @@ def main():
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
             "traffic": counter_traffic("decode_fast_kernel") if cfg == 4 else None,
         },
+        "token_granular_view": tokmode,
+        "stream_read_ceiling": ceiling,
+        "context_sweep_table2": sweep,
+        "tp4_per_gpu_share": share,
         "kv_maintenance": maint,
         "accept_top3": accept,
         "phase_cost_model": phase,

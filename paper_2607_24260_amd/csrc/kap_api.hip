@@ -2,6 +2,7 @@
 // workspace sizing and kernel dispatch. Nothing here allocates, frees or
 // synchronises; every launch goes to the caller's stream.
 #include "kap.h"
+#include "kap_diag.h"
 
 #include <cstdarg>
 #include <cstdio>
@@ -770,4 +771,20 @@ kap_status kap_accept_top3(int32_t batch, int32_t window, int32_t vocab, const v
   return ok();
 }
 
+// ---------------------------------------------------------------------------
+// kap_stream_read (measurement helper)
+// ---------------------------------------------------------------------------
+
+kap_status kap_stream_read(const void *src, size_t bytes, uint32_t *sink, void *stream) {
+  if (bytes == 0) return ok();
+  if (!src || !sink) return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (!aligned(src, 16) || bytes % 16 != 0)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "src must be 16-byte aligned and bytes a multiple of 16");
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_stream_read(src, bytes, sink, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(KAP_ERR_HIP, "stream_read launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // extern "C"
+

@@ -143,6 +143,7 @@ hipError_t launch_attn_generic(const AttnArgs &a, hipStream_t s);
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s);
 hipError_t launch_verify_mfma(const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(const AttnArgs &a, hipStream_t s);
+hipError_t launch_stream_read(const void *src, size_t bytes, uint32_t *sink, hipStream_t s);
 
 // Workgroups of the tuned kernels that fit on one compute unit at once
 // (0 if the runtime cannot tell).

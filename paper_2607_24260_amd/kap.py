@@ -47,6 +47,7 @@ EXPORTS = (
     "kap_append_kv", "kap_compact_view", "kap_fallback_update",
     "kap_accept_top3", "kap_accept_top3_workspace_bytes",
     "kap_status_string", "kap_last_error", "kap_abi_version",
+    "kap_stream_read",
 )
 
 
@@ -130,6 +131,8 @@ def load_library(path: str = LIB_PATH):
     lib.kap_accept_top3.argtypes = [_I32, _I32, _I32, _P, _I32, _P, _I32, _P, _P, _P, _SZ, _P]
     lib.kap_accept_top3_workspace_bytes.restype = _SZ
     lib.kap_accept_top3_workspace_bytes.argtypes = [_I32, _I32]
+    lib.kap_stream_read.restype = _I32
+    lib.kap_stream_read.argtypes = [_P, _SZ, _P, _P]
     lib.kap_status_string.restype = ctypes.c_char_p
     lib.kap_status_string.argtypes = [_I32]
     lib.kap_last_error.restype = ctypes.c_char_p
@@ -555,6 +558,18 @@ def verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scal
         _ptr(out), _ptr(lse), _ptr(workspace), have, _stream(stream))
     _check(st)
     return out, lse
+
+
+def stream_read(buf, sink, stream=None):
+    """kap_stream_read (measurement helper): read every byte of the device
+    tensor ``buf`` once with a plain streaming kernel, XOR-folding its words
+    into the int32 device scalar ``sink``."""
+    _dev(buf, "buf")
+    _dev(sink, "sink", torch.int32)
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    _check(load_library().kap_stream_read(_ptr(buf), buf.numel() * buf.element_size(),
+                                          _ptr(sink), _stream(stream)))
 
 
 def abi_version() -> int:

@@ -219,10 +219,11 @@ def make_workload(config: int, device="cpu", replicas: int = 1, batch: Optional[
                   seq_len: Optional[int] = None, seed: Optional[int] = None,
                   n_decode: Optional[int] = None, n_verify: Optional[int] = None,
                   num_q_heads: int = 32, num_kv_heads: int = 8, head_dim: int = 128,
-                  with_kv: bool = True) -> Workload:
+                  with_kv: bool = True, budget_frac: Optional[float] = None) -> Workload:
     """Build workload ``config`` (1..5). ``batch`` / ``seq_len`` / step counts may
     be shrunk for tests; the recipe is otherwise unchanged. ``with_kv=False``
-    skips drawing the KV pools (plan-only use)."""
+    skips drawing the KV pools (plan-only use). ``budget_frac`` replaces the
+    budget fraction of workloads 2-4 (for sweeps over the retained ratio)."""
     seed = config_seed(config) if seed is None else seed
     rng = np.random.Generator(np.random.PCG64(seed))
     Hq, Hkv, D = num_q_heads, num_kv_heads, head_dim
@@ -296,6 +297,8 @@ def make_workload(config: int, device="cpu", replicas: int = 1, batch: Optional[
     else:
         raise ValueError(f"unknown workload {config}")
 
+    if budget_frac is not None and config in (2, 3, 4):
+        budget = budget_tokens(budget_frac, seq_lens)
     if n_decode is not None and config != 5:
         nd = n_decode
     if n_verify is not None and config != 5:

@@ -10,7 +10,7 @@ import pytest
 from paper_2607_24260_amd import kap as K
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "kap.h")
+HEADERS = [os.path.join(ROOT, "include", f) for f in ("kap.h", "kap_diag.h")]
 
 
 @pytest.fixture(scope="module")
@@ -21,7 +21,7 @@ def lib():
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(kap_[a-z0-9_]+)\s*\(", text)))
 
@@ -156,6 +156,13 @@ def test_token_granular_calls_reject_bad_arguments(lib):
     st = lib.kap_selected_decode_masked(ctypes.byref(kv), 0, FAKE, FAKE, FAKE, FAKE, FAKE, 8,
                                         FAKE, 8, 1.0, 0, FAKE, FAKE, None, 0, None)
     assert st == K.KAP_OK
+
+
+def test_stream_read_rejects_bad_arguments(lib):
+    assert lib.kap_stream_read(FAKE, 0, None, None) == K.KAP_OK
+    assert lib.kap_stream_read(None, 64, FAKE, None) == K.KAP_ERR_INVALID_ARGUMENT
+    assert lib.kap_stream_read(FAKE + 4, 64, FAKE, None) == K.KAP_ERR_INVALID_ARGUMENT
+    assert lib.kap_stream_read(FAKE, 40, FAKE, None) == K.KAP_ERR_INVALID_ARGUMENT
 
 
 def test_binding_refuses_cpu_tensors():
