@@ -354,6 +354,24 @@ kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int
                                int32_t *view_num_blocks, int32_t view_stride, void *stream);
 
 /*
+ * kap_fallback_update_masked -- kap_fallback_update for token-granular views
+ * (kap_compile_plan_masked / kap_selected_decode_masked): whenever a
+ * sequence's active view row is written, its token-mask row is written too --
+ * view_token_mask[b][k] = sel_token_mask[b][k] in mode 0, 0xFFFF (every token
+ * of the page) in mode 1. sel_token_mask is [batch][sel_stride] and
+ * view_token_mask [batch][view_stride], uint32 (NULL only with a zero
+ * stride). Every other argument and error is that of kap_fallback_update.
+ */
+kap_status kap_fallback_update_masked(
+    int32_t batch, int32_t reset, int32_t window, int32_t gamma, const int32_t *accepted,
+    const int32_t *view_tokens, const int32_t *seq_lens, const int32_t *plan_status,
+    int32_t *history, int32_t *cycles, int32_t *mode, const int32_t *sel_block_table,
+    const int32_t *sel_logical_block, const uint32_t *sel_token_mask,
+    const int32_t *sel_num_blocks, int32_t sel_stride, const int32_t *full_block_table,
+    int32_t full_stride, int32_t *view_block_table, int32_t *view_logical_block,
+    uint32_t *view_token_mask, int32_t *view_num_blocks, int32_t view_stride, void *stream);
+
+/*
  * kap_accept_top3 -- target-guided tolerant acceptance of a verify window
  * (Sec. 3.2 "Full-context verification": a proposed token is accepted when it
  * lies within the full-context verifier's top candidates -- top 3 in the

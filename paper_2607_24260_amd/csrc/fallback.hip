@@ -6,8 +6,9 @@
 //
 // One workgroup per sequence: thread 0 updates the sequence's history and
 // mode; then the workgroup rewrites the sequence's active view row if its
-// mode was (re)set. h <= s is compared exactly, in integers:
-// A * seq_len <= view_tokens * S.
+// mode was (re)set (with token-granular views, also its token-mask row: the
+// plan's masks, or all 16 tokens of every page on full context). h <= s is
+// compared exactly, in integers: A * seq_len <= view_tokens * S.
 #include "kap_internal.h"
 
 namespace kap {
@@ -63,6 +64,11 @@ __global__ __launch_bounds__(kThreads) void fallback_update_kernel(FallbackArgs 
       vbt[j] = sbt[j];
       vlb[j] = slb[j];
     }
+    if (a.view_mask) {
+      const uint32_t *smk = a.sel_mask + (size_t)b * a.sel_stride;
+      uint32_t *vmk = a.view_mask + (size_t)b * a.view_stride;
+      for (int j = threadIdx.x; j < n; j += kThreads) vmk[j] = smk[j];
+    }
     if (threadIdx.x == 0) a.view_nb[b] = nb;
   } else {
     const int L = a.seq_lens[b];
@@ -72,6 +78,10 @@ __global__ __launch_bounds__(kThreads) void fallback_update_kernel(FallbackArgs 
     for (int j = threadIdx.x; j < n; j += kThreads) {
       vbt[j] = fbt[j];
       vlb[j] = j;
+    }
+    if (a.view_mask) {
+      uint32_t *vmk = a.view_mask + (size_t)b * a.view_stride;
+      for (int j = threadIdx.x; j < n; j += kThreads) vmk[j] = 0xFFFFu;
     }
     if (threadIdx.x == 0) a.view_nb[b] = n;
   }

@@ -666,15 +666,18 @@ kap_status kap_compact_view(const kap_kv_cache *src, int32_t batch,
   return ok();
 }
 
-kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int32_t gamma,
-                               const int32_t *accepted, const int32_t *view_tokens,
-                               const int32_t *seq_lens, const int32_t *plan_status,
-                               int32_t *history, int32_t *cycles, int32_t *mode,
-                               const int32_t *sel_block_table, const int32_t *sel_logical_block,
-                               const int32_t *sel_num_blocks, int32_t sel_stride,
-                               const int32_t *full_block_table, int32_t full_stride,
-                               int32_t *view_block_table, int32_t *view_logical_block,
-                               int32_t *view_num_blocks, int32_t view_stride, void *stream) {
+static kap_status fallback_update(int32_t batch, int32_t reset, int32_t window, int32_t gamma,
+                                  const int32_t *accepted, const int32_t *view_tokens,
+                                  const int32_t *seq_lens, const int32_t *plan_status,
+                                  int32_t *history, int32_t *cycles, int32_t *mode,
+                                  const int32_t *sel_block_table,
+                                  const int32_t *sel_logical_block,
+                                  const uint32_t *sel_token_mask, const int32_t *sel_num_blocks,
+                                  int32_t sel_stride, const int32_t *full_block_table,
+                                  int32_t full_stride, int32_t *view_block_table,
+                                  int32_t *view_logical_block, uint32_t *view_token_mask,
+                                  bool masked, int32_t *view_num_blocks, int32_t view_stride,
+                                  void *stream) {
   if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
   if (batch > 0x7fffffff / 2) return fail(KAP_ERR_UNSUPPORTED, "batch too large");
   if (window < 1 || window > 64) return fail(KAP_ERR_INVALID_ARGUMENT, "window %d outside [1, 64]", window);
@@ -691,6 +694,8 @@ kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int
       (full_stride > 0 && !full_block_table) ||
       (view_stride > 0 && (!view_block_table || !view_logical_block)))
     return fail(KAP_ERR_INVALID_ARGUMENT, "a table is NULL");
+  if (masked && ((sel_stride > 0 && !sel_token_mask) || (view_stride > 0 && !view_token_mask)))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a token-mask table is NULL");
   kap::FallbackArgs a;
   a.batch = batch;
   a.reset = reset != 0;
@@ -713,10 +718,45 @@ kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int
   a.view_lb = view_logical_block;
   a.view_nb = view_num_blocks;
   a.view_stride = view_stride;
+  if (masked && view_stride > 0) {
+    a.sel_mask = sel_token_mask;
+    a.view_mask = view_token_mask;
+  }
   (void)hipGetLastError();
   const hipError_t e = kap::launch_fallback_update(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(KAP_ERR_HIP, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+kap_status kap_fallback_update(int32_t batch, int32_t reset, int32_t window, int32_t gamma,
+                               const int32_t *accepted, const int32_t *view_tokens,
+                               const int32_t *seq_lens, const int32_t *plan_status,
+                               int32_t *history, int32_t *cycles, int32_t *mode,
+                               const int32_t *sel_block_table, const int32_t *sel_logical_block,
+                               const int32_t *sel_num_blocks, int32_t sel_stride,
+                               const int32_t *full_block_table, int32_t full_stride,
+                               int32_t *view_block_table, int32_t *view_logical_block,
+                               int32_t *view_num_blocks, int32_t view_stride, void *stream) {
+  return fallback_update(batch, reset, window, gamma, accepted, view_tokens, seq_lens,
+                         plan_status, history, cycles, mode, sel_block_table, sel_logical_block,
+                         nullptr, sel_num_blocks, sel_stride, full_block_table, full_stride,
+                         view_block_table, view_logical_block, nullptr, false, view_num_blocks,
+                         view_stride, stream);
+}
+
+kap_status kap_fallback_update_masked(
+    int32_t batch, int32_t reset, int32_t window, int32_t gamma, const int32_t *accepted,
+    const int32_t *view_tokens, const int32_t *seq_lens, const int32_t *plan_status,
+    int32_t *history, int32_t *cycles, int32_t *mode, const int32_t *sel_block_table,
+    const int32_t *sel_logical_block, const uint32_t *sel_token_mask,
+    const int32_t *sel_num_blocks, int32_t sel_stride, const int32_t *full_block_table,
+    int32_t full_stride, int32_t *view_block_table, int32_t *view_logical_block,
+    uint32_t *view_token_mask, int32_t *view_num_blocks, int32_t view_stride, void *stream) {
+  return fallback_update(batch, reset, window, gamma, accepted, view_tokens, seq_lens,
+                         plan_status, history, cycles, mode, sel_block_table, sel_logical_block,
+                         sel_token_mask, sel_num_blocks, sel_stride, full_block_table,
+                         full_stride, view_block_table, view_logical_block, view_token_mask, true,
+                         view_num_blocks, view_stride, stream);
 }
 
 // Workspace of kap_accept_top3: [row_best u64 x rows][row_count i32 x rows].

@@ -121,6 +121,10 @@ struct FallbackArgs {
   int full_stride;
   int32_t *view_bt, *view_lb, *view_nb;
   int view_stride;
+  // token-granular views: the plan's and the active row's token masks, laid
+  // out like the tables (NULL: page-granular)
+  const uint32_t *sel_mask = nullptr;
+  uint32_t *view_mask = nullptr;
 };
 
 // kap_accept_top3 after host validation.

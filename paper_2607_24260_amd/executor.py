@@ -191,7 +191,9 @@ class DeviceStream:
     Accept lengths per cycle come in as device arrays uploaded once (here the
     seeded draws; the kernel clamps them to gamma). ``plan`` holds the
     compiled plan tensors; ``plan_call``, if given, recompiles the plan at
-    the start of every stream."""
+    the start of every stream. A token-granular plan (one with
+    ``view_token_mask``, Sec. 3.1's visibility mask at token resolution) runs
+    with masked decode calls and a masked fallback switch."""
 
     def __init__(self, w, kv, plan: dict, *, window: int = 4, plan_call=None, stream=None):
         import torch
@@ -212,6 +214,10 @@ class DeviceStream:
         self.vbt = torch.zeros((B, stride), dtype=torch.int32, device=dev)
         self.vlb = torch.zeros((B, stride), dtype=torch.int32, device=dev)
         self.vnb = torch.zeros(B, dtype=torch.int32, device=dev)
+        tok = "view_token_mask" in plan
+        self.vmask = torch.zeros((B, stride), dtype=torch.int32, device=dev) if tok else None
+        masks = dict(sel_token_mask=plan["view_token_mask"], view_token_mask=self.vmask) \
+            if tok else {}
         self.history = torch.zeros((B, window, 2), dtype=torch.int32, device=dev)
         self.cycles = torch.zeros(B, dtype=torch.int32, device=dev)
         self.mode = torch.zeros(B, dtype=torch.int32, device=dev)
@@ -221,8 +227,9 @@ class DeviceStream:
                   self.cycles, self.mode, plan["view_block_table"], plan["view_logical_block"],
                   plan["view_num_blocks"], self.fbt, self.vbt, self.vlb, self.vnb)
         s = self.stream
-        self.reset = K.bind_fallback_update(True, window, 0, None, *common, stream=s)
-        self.update = [K.bind_fallback_update(False, window, g, self.draws[c], *common, stream=s)
+        self.reset = K.bind_fallback_update(True, window, 0, None, *common, stream=s, **masks)
+        self.update = [K.bind_fallback_update(False, window, g, self.draws[c], *common, stream=s,
+                                              **masks)
                        for c, g in enumerate(self.gammas)]
         Hq, D = w.num_q_heads, w.head_dim
         self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
@@ -231,7 +238,7 @@ class DeviceStream:
                          dtype=torch.uint8, device=dev)
         self.decode = [K.bind_selected_decode(kv, w.q_decode[i], self.seq_lens, self.vbt,
                                               self.vlb, self.vnb, stride, w.sm_scale, self.out,
-                                              self.lse, ws, stream=s)
+                                              self.lse, ws, view_token_mask=self.vmask, stream=s)
                        for i in range(w.q_decode.shape[0])]
         max_len = int(np.max(w.seq_lens))
         self.ver_out, self.verify = [], []

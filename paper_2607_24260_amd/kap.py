@@ -44,7 +44,7 @@ EXPORTS = (
     "kap_compile_plan", "kap_compile_plan_workspace_bytes", "kap_compile_plan_masked",
     "kap_selected_decode", "kap_selected_decode_workspace_bytes", "kap_selected_decode_masked",
     "kap_verify", "kap_verify_workspace_bytes",
-    "kap_append_kv", "kap_compact_view", "kap_fallback_update",
+    "kap_append_kv", "kap_compact_view", "kap_fallback_update", "kap_fallback_update_masked",
     "kap_accept_top3", "kap_accept_top3_workspace_bytes",
     "kap_status_string", "kap_last_error", "kap_abi_version",
     "kap_stream_read",
@@ -127,6 +127,10 @@ def load_library(path: str = LIB_PATH):
     lib.kap_fallback_update.argtypes = [
         _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32,
         _P, _P, _P, _I32, _P]
+    lib.kap_fallback_update_masked.restype = _I32
+    lib.kap_fallback_update_masked.argtypes = [
+        _I32, _I32, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I32, _P, _I32,
+        _P, _P, _P, _P, _I32, _P]
     lib.kap_accept_top3.restype = _I32
     lib.kap_accept_top3.argtypes = [_I32, _I32, _I32, _P, _I32, _P, _I32, _P, _P, _P, _SZ, _P]
     lib.kap_accept_top3_workspace_bytes.restype = _SZ
@@ -292,10 +296,13 @@ def compact_view(src: KVCache, view_block_table, view_num_blocks, view_capacity:
 def bind_fallback_update(reset: bool, window: int, gamma: int, accepted, view_tokens, seq_lens,
                          plan_status, history, cycles, mode, sel_block_table, sel_logical_block,
                          sel_num_blocks, full_block_table, view_block_table, view_logical_block,
-                         view_num_blocks, stream=None) -> "BoundCall":
+                         view_num_blocks, sel_token_mask=None, view_token_mask=None,
+                         stream=None) -> "BoundCall":
     """One cycle of the device-side access-mode policy (kap_fallback_update),
     marshalled once; see kap.h. All arrays int32 on the GPU; history
-    [B][window][2], the tables [B][stride]."""
+    [B][window][2], the tables [B][stride]. With the two token-mask tables
+    (token-granular views, shaped like the sel_ / view_ tables) it calls
+    kap_fallback_update_masked."""
     lib = load_library()
     B = int(seq_lens.shape[0])
     named = dict(view_tokens=view_tokens, seq_lens=seq_lens, plan_status=plan_status,
@@ -321,17 +328,28 @@ def bind_fallback_update(reset: bool, window: int, gamma: int, accepted, view_to
     if sel_logical_block.shape != sel_block_table.shape or \
             view_logical_block.shape != view_block_table.shape:
         raise ValueError("block and logical-block tables must have the same shape")
+    masked = sel_token_mask is not None or view_token_mask is not None
+    if masked:
+        for name, t, like in (("sel_token_mask", sel_token_mask, sel_block_table),
+                              ("view_token_mask", view_token_mask, view_block_table)):
+            _dev(t, name, torch.int32, 2)
+            if t.shape != like.shape:
+                raise ValueError(f"{name} must be shaped like its block table")
+    mask = lambda t: (_ptr(t),) if masked else ()
     args = (B, int(bool(reset)), int(window), int(gamma), _ptr(accepted), _ptr(view_tokens),
             _ptr(seq_lens), _ptr(plan_status), _ptr(history), _ptr(cycles), _ptr(mode),
-            _ptr(sel_block_table), _ptr(sel_logical_block), _ptr(sel_num_blocks),
-            sel_block_table.shape[1], _ptr(full_block_table), full_block_table.shape[1],
-            _ptr(view_block_table), _ptr(view_logical_block), _ptr(view_num_blocks),
-            view_block_table.shape[1], _stream(stream))
+            _ptr(sel_block_table), _ptr(sel_logical_block), *mask(sel_token_mask),
+            _ptr(sel_num_blocks), sel_block_table.shape[1], _ptr(full_block_table),
+            full_block_table.shape[1], _ptr(view_block_table), _ptr(view_logical_block),
+            *mask(view_token_mask), _ptr(view_num_blocks), view_block_table.shape[1],
+            _stream(stream))
     # not run here: the call updates state (errors surface when it is called)
-    return BoundCall(lib.kap_fallback_update, args,
+    fn = lib.kap_fallback_update_masked if masked else lib.kap_fallback_update
+    return BoundCall(fn, args,
                      (accepted, view_tokens, seq_lens, plan_status, history, cycles, mode,
                       sel_block_table, sel_logical_block, sel_num_blocks, full_block_table,
-                      view_block_table, view_logical_block, view_num_blocks))
+                      view_block_table, view_logical_block, view_num_blocks, sel_token_mask,
+                      view_token_mask))
 
 
 # --------------------------------------------------------------------------

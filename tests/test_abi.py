@@ -165,6 +165,16 @@ def test_stream_read_rejects_bad_arguments(lib):
     assert lib.kap_stream_read(FAKE, 40, FAKE, None) == K.KAP_ERR_INVALID_ARGUMENT
 
 
+def test_masked_fallback_rejects_missing_masks(lib):
+    # token-mask tables are required whenever their stride is non-zero
+    args = [2, 1, 4, 0, None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 8,
+            FAKE, 8, FAKE, FAKE, FAKE, FAKE, 8, None]
+    assert lib.kap_fallback_update_masked(*args) == K.KAP_ERR_INVALID_ARGUMENT
+    assert b"token-mask" in lib.kap_last_error()
+    args[0] = 0
+    assert lib.kap_fallback_update_masked(*args) == K.KAP_OK
+
+
 def test_binding_refuses_cpu_tensors():
     import torch
     with pytest.raises(ValueError, match="GPU tensor"):

@@ -178,6 +178,23 @@ def test_balanced_map_beyond_64_sequences():
     verify_check(w, pool, [0], batches=[0, 64, 99], kv_heads=[0, 7])
 
 
+@pytest.mark.parametrize("seq_len,frac", [(4096, 0.401), (16384, 0.242), (65536, 0.108)])
+def test_table2_context_buckets(seq_len, frac):
+    # the bench's context sweep shapes (B = 4, the bucket's retained ratio as
+    # the budget): decode on every sequence, verify on sequences {0, 3} x KV
+    # heads {0, 4}
+    w, pool = workload(4, seq_len=seq_len, budget_frac=frac, n_decode=1, n_verify=1)
+    decode_check(w, pool, [0])
+    verify_check(w, pool, [0], batches=[0, 3], kv_heads=[0, 4])
+
+
+def test_head_split_share():
+    # one GPU's share of a 4-way head split at 128K: 8 query / 2 KV heads
+    w, pool = workload(4, num_q_heads=8, num_kv_heads=2, n_decode=1, n_verify=1)
+    decode_check(w, pool, [0])
+    verify_check(w, pool, [0], batches=[1, 2])
+
+
 # --------------------------------------------------------------------------
 # cross-checks and edge cases on small shapes (several tiles + ragged tails)
 # --------------------------------------------------------------------------

@@ -121,3 +121,67 @@ def test_device_stream_equals_host_policy_stream():
         assert torch.equal(o, ds.ver_out[j][0]) and torch.equal(l, ds.ver_out[j][1]), j
     (idx, o, l, _), = res.decode_out
     assert idx == last and torch.equal(o, ds.out) and torch.equal(l, ds.lse)
+
+
+def test_token_granular_device_stream():
+    # the ragged fp8 stream over token-granular views (NEXT 3 in the
+    # device-resident cycle): modes follow the host policy with the token
+    # plan's s; every active row holds the plan's pages and masks (mode 0) or
+    # the full table with all-ones masks (mode 1); the last decode equals a
+    # masked call over those rows and, for sampled sequences, the oracle
+    from oracle import kap_oracle as O
+
+    from kap_testlib import LSE_TOL, O_TOL, assert_close, oracle_pool
+
+    # 4 cycles: long enough for some sequences to fall back, short enough
+    # that others keep their views under the recipe's accept law
+    w = make_workload(5, device="cuda", batch=16, seq_len=65536, n_verify=4)
+    kv = kv_of(w)
+    cap = w.max_pages_per_seq
+    plan = K.compile_plan(
+        dev_i32(w.seq_lens), dev_i32(w.full_block_table), dev_i32(w.span_offsets),
+        dev_i32(w.span_start), dev_i32(w.span_len),
+        torch.as_tensor(np.asarray(w.span_prior, dtype=np.float32)).cuda(), dev_i32(w.prefix),
+        dev_i32(w.suffix), dev_i32(w.budget), num_pages=w.num_pages, view_capacity=cap,
+        token_granular=True)
+    ds = DeviceStream(w, kv, plan)
+    ds.run()
+    torch.cuda.synchronize()
+    L = np.asarray(w.seq_lens, dtype=np.int64)
+    vt = plan["view_tokens"].cpu().numpy()
+    ok = plan["plan_status"].cpu().numpy() == K.KAP_PLAN_OK
+    policy = FallbackPolicy(vt / L.astype(np.float64), ok, window=4)
+    draws = np.asarray(w.accept_draws)
+    for c, q in enumerate(w.q_verify):
+        g = q.shape[1] - 1
+        policy.update(accepted_counts(draws[c], g), g)
+    mode = ds.mode.cpu().numpy()
+    assert np.array_equal(mode, policy.mode)
+    assert (mode == 0).any() and (mode == FULL).any(), "want both access modes in the stream"
+    vnb, vbt = ds.vnb.cpu().numpy(), ds.vbt.cpu().numpy()
+    vlb, vmk = ds.vlb.cpu().numpy(), ds.vmask.cpu().numpy().astype(np.int64) & 0xFFFFFFFF
+    pbt, plb = plan["view_block_table"].cpu().numpy(), plan["view_logical_block"].cpu().numpy()
+    pmk = plan["view_token_mask"].cpu().numpy().astype(np.int64) & 0xFFFFFFFF
+    pnb = plan["view_num_blocks"].cpu().numpy()
+    fbt = np.asarray(w.full_block_table)
+    for b in range(w.batch):
+        n = int(vnb[b])
+        if mode[b] == 0:
+            assert n == pnb[b]
+            assert np.array_equal(vbt[b, :n], pbt[b, :n]) and np.array_equal(vlb[b, :n], plb[b, :n])
+            assert np.array_equal(vmk[b, :n], pmk[b, :n]), b
+        else:
+            assert n == -(-L[b] // 16)
+            assert np.array_equal(vbt[b, :n], fbt[b, :n]) and np.all(vmk[b, :n] == 0xFFFF), b
+    last = w.q_decode.shape[0] - 1
+    o, l = K.selected_decode(kv, w.q_decode[last], ds.seq_lens, ds.vbt, ds.vlb, ds.vnb,
+                             ds.vbt.shape[1], w.sm_scale, view_token_mask=ds.vmask)
+    torch.cuda.synchronize()
+    assert torch.equal(o, ds.out) and torch.equal(l, ds.lse)
+    sel = [b for b in range(w.batch) if mode[b] == 0][:2] + [b for b in range(w.batch)
+                                                              if mode[b] == FULL][:2]
+    eo, el = O.selected_decode(oracle_pool(w), w.q_decode[last].float().cpu().numpy()[sel],
+                               L[sel], vbt[sel], vlb[sel], vnb[sel], w.sm_scale,
+                               view_token_mask=vmk[sel])
+    assert_close("token stream O", o.cpu().numpy()[sel], eo, O_TOL)
+    assert_close("token stream LSE", l.cpu().numpy()[sel], el, LSE_TOL)
