@@ -7,11 +7,12 @@
 //   3. ranks the spans by (prior desc, start asc, index asc) -- every thread
 //      counts, for its spans, how many spans precede them, and writes the
 //      inverse permutation to the workspace,
-//   4. walks the spans in rank order with one wavefront: the 64 lanes test the
-//      span against the bitmap, a wavefront reduction counts what is new (its
-//      cost in visible tokens), and the span is taken when it fits the budget,
-//   5. compacts the bitmap into the ascending logical-page list and maps it
-//      through the full block table.
+//   4. walks the spans in rank order with one wavefront, 64 at a time: each
+//      lane prices its span against the bitmap (its cost in visible tokens),
+//      a ballot finds the first span that fits, and only a taken span changes
+//      the state -- one round per taken span, not per span,
+//   5. compacts the bitmap into the ascending logical-page list (staged in
+//      LDS) and maps it through the full block table.
 // Page mode keeps one bit per page; token mode (the visibility mask of
 // Sec. 3.1 at token resolution) one bit per token, and also emits each view
 // page's 16-bit mask of visible tokens.
@@ -22,25 +23,19 @@
 namespace kap {
 namespace {
 
-constexpr int kRankChunk = 1024;
+constexpr int kRankChunk = 2048;   // ranking keys staged per pass; also the LDS view list
 
-__device__ __forceinline__ bool ranks_before(float pj, int sj, int j, float pi, int si, int i) {
-  if (pj > pi) return true;
-  if (pj < pi) return false;           // equal values (including -0 == +0) fall through
-  if (sj != si) return sj < si;
-  return j < i;
+// Branch-free: equal priors (including -0 == +0) fall through to the start,
+// then to the index.
+__device__ __forceinline__ int ranks_before(float pj, int sj, int j, float pi, int si, int i) {
+  return (pj > pi) | ((pj == pi) & ((sj < si) | ((sj == si) & (j < i))));
 }
 
 // Exclusive prefix sum of v over the workgroup (kPlanThreads threads, in
 // thread order); *total receives the sum. s_tmp holds kPlanThreads/64 ints.
 __device__ __forceinline__ int block_exclusive_scan(int v, int *s_tmp, int *total) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_scan_add(v);                      // inclusive, within the wavefront
   if (lane == 63) s_tmp[w] = x;
   __syncthreads();
   int before = 0, all = 0;
@@ -54,19 +49,11 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int *s_tmp, int *tota
   return before + x - v;
 }
 
-// Bits of token word w (tokens 32w .. 32w + 31) that lie in [x, e).
+// Bits of bitmap word w (bits 32w .. 32w + 31) that lie in [x, e).
 __device__ __forceinline__ uint32_t range_bits(int w, int x, int e) {
   const int lo = min(max(x - 32 * w, 0), 32);
   const int hi = min(max(e - 32 * w, 0), 32);
   return (uint32_t)(((1ull << hi) - 1ull) ^ ((1ull << lo) - 1ull));
-}
-
-// Sum over the wavefront of a per-lane count in [0, 63]: one ballot per bit.
-__device__ __forceinline__ int wave_count_sum(int c) {
-  int s = 0;
-#pragma unroll
-  for (int k = 0; k < 6; ++k) s += __popcll(__ballot((c >> k) & 1)) << k;
-  return s;
 }
 
 template <bool TOK>
@@ -76,8 +63,8 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __shared__ int s_scan[kPlanThreads / 64];
   __shared__ long long s_used;
   __shared__ int s_taken;
-  __shared__ float s_prior[kRankChunk];
-  __shared__ int s_start[kRankChunk];
+  __shared__ __align__(16) float s_prior[kRankChunk];
+  __shared__ __align__(16) int s_start[kRankChunk];
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -109,11 +96,30 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     return;
   }
 
-  // -- scores ---------------------------------------------------------------
+  // -- scores, and the first chunk of ranking keys -----------------------------
+  // Keys are staged in LDS padded to a multiple of four with keys that rank
+  // after every span (prior -inf, start INT_MAX, index >= n).
+  const int n = hi - lo;
+  const bool one_chunk = n <= kRankChunk;
   if (tid == 0) s_flag = 0;
   __syncthreads();
-  for (int i = lo + tid; i < hi; i += kPlanThreads)
-    if (__builtin_isnan(a.span_prior[i])) s_flag = 1;
+  {
+    const int jn4 = (min(n, kRankChunk) + 3) & ~3;
+    const int lim = max(n, jn4);
+    for (int t = tid; t < lim; t += kPlanThreads) {
+      if (t < n) {
+        const float pr = a.span_prior[lo + t];
+        if (__builtin_isnan(pr)) s_flag = 1;
+        if (t < kRankChunk) {
+          s_prior[t] = pr;
+          s_start[t] = a.span_start[lo + t];
+        }
+      } else {
+        s_prior[t] = -INFINITY;
+        s_start[t] = 0x7fffffff;
+      }
+    }
+  }
   __syncthreads();
   if (s_flag) {
     write_fail(2 /*KAP_PLAN_BAD_SCORE*/, true);
@@ -139,25 +145,41 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   }
 
   // -- rank the spans ---------------------------------------------------------
-  // rank(i) = number of spans ordered before span i; keys are staged through
-  // LDS in chunks of kRankChunk so the all-pairs count reads LDS broadcasts.
-  const int n = hi - lo;
+  // rank(i) = number of spans ordered before span i; keys are read from LDS in
+  // chunks of kRankChunk (a single chunk, staged above, in the common case),
+  // four per broadcast read.
   for (int ib = 0; ib < n; ib += kPlanThreads) {
     const int i = ib + tid;
     const bool act = i < n;
-    const float pi = act ? a.span_prior[lo + i] : 0.f;
-    const int si = act ? a.span_start[lo + i] : 0;
+    float pi = 0.f;
+    int si = 0;
+    if (act) {
+      pi = one_chunk ? s_prior[i] : a.span_prior[lo + i];
+      si = one_chunk ? s_start[i] : a.span_start[lo + i];
+    }
     int rank = 0;
     for (int jb = 0; jb < n; jb += kRankChunk) {
-      __syncthreads();
       const int jn = min(kRankChunk, n - jb);
-      for (int t = tid; t < jn; t += kPlanThreads) {
-        s_prior[t] = a.span_prior[lo + jb + t];
-        s_start[t] = a.span_start[lo + jb + t];
+      const int jn4 = (jn + 3) & ~3;
+      if (!one_chunk) {
+        __syncthreads();
+        for (int t = tid; t < jn4; t += kPlanThreads) {
+          const bool real = t < jn;
+          s_prior[t] = real ? a.span_prior[lo + jb + t] : -INFINITY;
+          s_start[t] = real ? a.span_start[lo + jb + t] : 0x7fffffff;
+        }
+        __syncthreads();
       }
-      __syncthreads();
-      if (act)
-        for (int t = 0; t < jn; ++t) rank += ranks_before(s_prior[t], s_start[t], jb + t, pi, si, i);
+      if (act) {
+#pragma unroll 4
+        for (int t = 0; t < jn4; t += 4) {
+          const float4 p4 = *reinterpret_cast<const float4 *>(&s_prior[t]);
+          const int4 s4 = *reinterpret_cast<const int4 *>(&s_start[t]);
+          const int j = jb + t;
+          rank += ranks_before(p4.x, s4.x, j, pi, si, i) + ranks_before(p4.y, s4.y, j + 1, pi, si, i) +
+                  ranks_before(p4.z, s4.z, j + 2, pi, si, i) + ranks_before(p4.w, s4.w, j + 3, pi, si, i);
+        }
+      }
     }
     if (act) {
       a.perm[lo + rank] = i;
@@ -186,68 +208,78 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __syncthreads();
 
   // -- greedy selection in rank order (one wavefront) -------------------------
-  // Lane l holds the clipped span of rank r0 + l, so one global round trip
-  // serves 64 decisions. Page mode: every page except the last (always
-  // selected) holds 16 tokens, so a span costs 16 x (its pages not yet
-  // selected), counted with a ballot over 64 pages at a time. Token mode: a
-  // span costs its tokens not yet visible, 64 bitmap words at a time.
+  // The spans are walked 64 ranks at a time, lane l holding the span of rank
+  // r0 + l as a bit range [u0, u1) of the bitmap (pages; tokens in token mode)
+  // and its count of bits not yet set. The state changes only when a span is
+  // taken, so every span between two taken ones is decided against the same
+  // state: a ballot finds the first span (in rank order) that fits, the ones
+  // before it are rejected (SKIP) or, if one of them fails, selection ends
+  // (STOP). When span j is taken, each later lane whose range meets j's
+  // subtracts the bits j newly covers (read before j's bits are set), so a
+  // batch costs one round per taken span instead of one per span. Page mode:
+  // every page but the last (always selected) holds 16 tokens, so a span costs
+  // 16 per new page. The budget state is wavefront-uniform.
   if (tid < 64) {
-    long long used = s_used;
+    int used = __builtin_amdgcn_readfirstlane((int)s_used);
     int taken = 0;
-    const long long T = a.budget[b];
+    const int T = a.budget[b];
     bool stop = false;
     for (int r0 = 0; r0 < n && !stop; r0 += 64) {
-      int my_i = -1, my_x = 0, my_e = 0;
+      int my_i = -1, x = 0, e = 0;
       if (r0 + lane < n) {
         my_i = lo + a.perm[lo + r0 + lane];
         const long long st = a.span_start[my_i];
-        const long long x = st > 0 ? st : 0;
-        long long e = st + (long long)a.span_len[my_i];
-        if (e > L) e = L;
-        my_x = (int)x;
-        my_e = (int)(e > x ? e : x);                    // e <= x: empty after clipping
+        const long long x64 = st > 0 ? st : 0;
+        long long e64 = st + (long long)a.span_len[my_i];
+        if (e64 > L) e64 = L;
+        x = (int)x64;
+        e = (int)(e64 > x64 ? e64 : x64);               // e <= x: empty after clipping
       }
-      const int cnt = min(64, n - r0);
-      for (int j = 0; j < cnt; ++j) {
-        const int i = __builtin_amdgcn_readlane(my_i, j);
-        const int x = __builtin_amdgcn_readlane(my_x, j);
-        const int e = __builtin_amdgcn_readlane(my_e, j);
-        if (e <= x) continue;                           // ignored
-        long long cost = 0;
-        int u0, u1;                                     // bitmap units (pages / words) touched
-        if constexpr (TOK) {
-          u0 = x >> 5;
-          u1 = ((e - 1) >> 5) + 1;
-          for (int w = u0 + lane; w - lane < u1; w += 64) {
-            const int c = w < u1 ? __popc(range_bits(w, x, e) & ~bitmap[w]) : 0;
-            cost += wave_count_sum(c);
-          }
-        } else {
-          u0 = x / kPage;
-          u1 = (e + kPage - 1) / kPage;
-          int new_pages = 0;
-          for (int p = u0; p < u1; p += 64) {
-            const int pp = p + lane;
-            const bool fresh = pp < u1 && !((bitmap[pp >> 5] >> (pp & 31)) & 1u);
-            new_pages += __popcll(__ballot(fresh));
-          }
-          cost = (long long)kPage * new_pages;
-        }
-        if (used + cost <= T) {
-          if constexpr (TOK) {
-            for (int w = u0 + lane; w < u1; w += 64) bitmap[w] |= range_bits(w, x, e);
-          } else {
-            for (int p = u0 + lane; p < u1; p += 64) atomicOr(&bitmap[p >> 5], 1u << (p & 31));
-          }
-          used += cost;
-          ++taken;
-          if (lane == 0 && a.span_selected) a.span_selected[i] = 1;
-        } else if (a.policy == 1 /*KAP_SELECT_STOP*/) {
+      const bool valid = e > x;                         // empty spans are ignored
+      const int u0 = TOK ? x : x / kPage;
+      const int u1 = TOK ? e : (e + kPage - 1) / kPage;
+      int fresh = 0;
+      if (valid)
+        for (int w = u0 >> 5; w <= (u1 - 1) >> 5; ++w)
+          fresh += __popc(range_bits(w, u0, u1) & ~bitmap[w]);
+      bool my_taken = false;
+      int pos = 0;                                      // lanes below pos are decided
+      while (true) {
+        const int cost = TOK ? fresh : kPage * fresh;
+        const bool open = valid && lane >= pos;
+        const bool fits = used + cost <= T;
+        const unsigned long long mf = __ballot(open && fits);
+        const unsigned long long mx = __ballot(open && !fits);
+        const int j = mf ? __builtin_ctzll(mf) : 64;
+        const int jx = mx ? __builtin_ctzll(mx) : 64;
+        if (a.policy == 1 /*KAP_SELECT_STOP*/ && jx < j) {
           stop = true;
           break;
         }
+        if (j == 64) break;
+        // take span j
+        const int ju0 = __builtin_amdgcn_readlane(u0, j);
+        const int ju1 = __builtin_amdgcn_readlane(u1, j);
+        used += __builtin_amdgcn_readlane(cost, j);
+        ++taken;
+        my_taken |= lane == j;
+        pos = j + 1;
+        const int c0 = max(u0, ju0), c1 = min(u1, ju1);
+        int delta = 0;
+        if (valid && lane > j && c0 < c1)
+          for (int w = c0 >> 5; w <= (c1 - 1) >> 5; ++w)
+            delta += __popc(range_bits(w, c0, c1) & ~bitmap[w]);
+        fresh -= delta;
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        const int jw0 = ju0 >> 5, jw1 = (ju1 - 1) >> 5;
+        for (int wb = jw0; wb <= jw1; wb += 64) {
+          const int w = wb + lane;
+          const bool in = w <= jw1;
+          atomicOr(&bitmap[in ? w : jw1], in ? range_bits(w, ju0, ju1) : 0u);
+        }
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       }
+      if (a.span_selected && my_taken) a.span_selected[my_i] = 1;
     }
     if (lane == 0) {
       s_used = used;
@@ -278,13 +310,25 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   const int32_t *fbt_row = a.fbt + (size_t)b * a.fbt_stride;
   int32_t *vbt = a.view_bt + (size_t)b * a.capacity;
   int32_t *vlb = a.view_lblk + (size_t)b * a.capacity;
+  uint32_t *vmk = TOK ? a.view_mask + (size_t)b * a.capacity : nullptr;
   bool bad = false;
+  // Views of up to kRankChunk pages: the logical pages (and masks) go to LDS
+  // at their output index first, then every thread maps entries k, k + 256,
+  // ... through the full block table, so the table reads are all in flight
+  // at once. Longer views map each page where it is found.
+  const bool staged = nblk <= kRankChunk;
+  uint32_t *s_lmask = reinterpret_cast<uint32_t *>(s_prior);
   auto emit = [&](int p, uint32_t mask) {
-    const int page = fbt_row[p];
-    bad |= (page < 0) || ((int64_t)page >= a.num_pages);
-    vlb[out] = p;
-    vbt[out] = page;
-    if constexpr (TOK) a.view_mask[(size_t)b * a.capacity + out] = mask;
+    if (staged) {
+      s_start[out] = p;
+      if constexpr (TOK) s_lmask[out] = mask;
+    } else {
+      const int page = fbt_row[p];
+      bad |= (page < 0) || ((int64_t)page >= a.num_pages);
+      vlb[out] = p;
+      vbt[out] = page;
+      if constexpr (TOK) vmk[out] = mask;
+    }
     ++out;
   };
   for (int w = w0; w < w1; ++w) {
@@ -299,6 +343,17 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
         bits &= bits - 1u;
         emit(w * 32 + bit, 0u);
       }
+    }
+  }
+  if (staged) {
+    __syncthreads();
+    for (int k = tid; k < nblk; k += kPlanThreads) {
+      const int p = s_start[k];
+      const int page = fbt_row[p];
+      bad |= (page < 0) || ((int64_t)page >= a.num_pages);
+      vlb[k] = p;
+      vbt[k] = page;
+      if constexpr (TOK) vmk[k] = s_lmask[k];
     }
   }
   if (bad) s_flag = 1;
