@@ -1,6 +1,6 @@
 """Plain fp64 CPU oracle for the KAP / GraphSpec selected-KV hot path.
 
-TEST INFRASTRUCTURE. This module is the checker, not the product: only the
+TEST INFRASTRUCTURE. This module is the oracle, not the product: only the
 test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import or call it. It shares no code, tables or helpers with
 the HIP library or its Python binding, and imports neither.
