@@ -124,7 +124,7 @@ def test_device_stream_equals_host_policy_stream():
 
 
 def test_token_granular_device_stream():
-    # the ragged fp8 stream over token-granular views (NEXT 3 in the
+    # the ragged fp8 stream over token-granular views (Sec. 3.1 mask in the
     # device-resident cycle): modes follow the host policy with the token
     # plan's s; every active row holds the plan's pages and masks (mode 0) or
     # the full table with all-ones masks (mode 1); the last decode equals a
