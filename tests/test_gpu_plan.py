@@ -151,3 +151,21 @@ def test_deterministic():
     for k in ("view_block_table", "view_logical_block"):   # entries past nblk are untouched
         for r in range(w.batch):
             assert torch.equal(a[k][r, :nb[r]], b[k][r, :nb[r]]), (k, r)
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+@pytest.mark.parametrize("frac", [0.3, 0.7, 1.0])
+def test_long_overlapping_spans_many_taken(policy, frac):
+    # 131072 tokens, 150 spans of up to the whole sequence (a span then covers
+    # up to 256 bitmap words), heavy overlap and many zero-cost spans; with a
+    # budget of the whole sequence every span is taken (one round each)
+    rng = np.random.default_rng(int(frac * 10) + 3 * policy)
+    L = 131072
+    stride = L // 16
+    spans = [(int(rng.integers(-1000, L)), int(rng.integers(1, L)), float(rng.choice([0.2, 0.5, rng.random()])))
+             for _ in range(150)]
+    spans += [(int(rng.integers(0, L - 64)), 64, 0.9) for _ in range(20)]
+    _, plans = run_both([L], [rng.permutation(stride)], [spans], [100], [50],
+                        [int(frac * L)], policy=policy)
+    if frac == 1.0 and policy == 0:
+        assert plans[0].spans_taken == sum(1 for s, n, _ in spans if min(L, s + n) > max(0, s))
