@@ -738,6 +738,12 @@ def main():
         },
         "token_granular_view": tokmode,
         "stream_read_ceiling": ceiling,
+        # the same calls against a plain streaming read of their size
+        "frac_of_read_ceiling": None if ceiling is None else {
+            "verify": round(ceiling["verify_size"]["us_per_call"] / (t_ver * 1e3)
+                            * ver_b / ceiling["verify_size"]["bytes"], 4),
+            "decode": round(ceiling["decode_size"]["us_per_call"] / (t_dec * 1e3)
+                            * dec_b / ceiling["decode_size"]["bytes"], 4)},
         "context_sweep_table2": sweep,
         "tp4_per_gpu_share": share,
         "kv_maintenance": maint,
