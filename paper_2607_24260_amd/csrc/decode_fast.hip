@@ -231,11 +231,19 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   const int32_t *vbt = a.block_table + (size_t)b * a.bt_stride;
   const int32_t *vlb = a.logical_block + (size_t)b * a.bt_stride;
   const uint32_t *vmk = MASKED ? a.token_mask + (size_t)b * a.bt_stride : nullptr;
-  auto table_read = [&](int i, int &raw_page, int &raw_lblk, uint32_t &raw_mask) {
-    const int kk = min(u + nw * i, last_entry);
-    raw_page = vbt[kk];
-    raw_lblk = vlb[kk];
-    raw_mask = MASKED ? vmk[kk] : 0xFFFFu;
+  // Entries of the pages a ring round ahead, read through the vector memory
+  // pipe (see table_ahead): issued when a ring slot is refilled, used when the
+  // slot is refilled next, one round later.
+  const int vz = opaque_zero();
+  const auto rbt = table_rsrc(vbt, last_entry + 1);
+  const auto rlb = table_rsrc(vlb, last_entry + 1);
+  const auto rmk = table_rsrc(MASKED ? reinterpret_cast<const int32_t *>(vmk) : vbt, last_entry + 1);
+  int ahead_pg[RING], ahead_lb[RING], ahead_mk[RING];
+  auto table_issue = [&](int entry, int j) {
+    const int kk = min(entry, last_entry);
+    ahead_pg[j] = table_ahead(rbt, vz, kk);
+    ahead_lb[j] = table_ahead(rlb, vz, kk);
+    ahead_mk[j] = MASKED ? table_ahead(rmk, vz, kk) : 0xFFFF;
   };
 
   // query slices of the four heads, as bf16 pairs matching the K slice
@@ -267,22 +275,20 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   // is invalid, the block lies past the sequence, or i is past this
   // wavefront's entries): tokens below the sequence length, and with a token
   // mask only those whose bit is set.
-  auto validate = [&](int i, int raw_page, int raw_lblk, uint32_t raw_mask, int &page,
+  auto validate = [&](bool live, int raw_page, int raw_lblk, uint32_t raw_mask, int &page,
                       uint32_t &vis) {
     const long long rem = (long long)L - (long long)raw_lblk * kPage;
     const int nvalid = (int)(rem < 0 ? 0 : (rem > kPage ? kPage : rem));
     vis = (0xFFFFu >> (kPage - nvalid)) & raw_mask;
     page = raw_page;
-    if (page < 0 || (int64_t)page >= a.num_pages || i >= n_my) {
+    if (page < 0 || (int64_t)page >= a.num_pages || !live) {
       vis = 0u;
       page = 0;
     }
   };
-  auto page_info = [&](int i, int &page, uint32_t &vis) {   // used only when n_my > 0
-    int rp, rl;
-    uint32_t rm;
-    table_read(i, rp, rl, rm);
-    validate(i, rp, rl, rm, page, vis);
+  auto page_info = [&](bool live, int j, int &page, uint32_t &vis) {   // entries from table_issue
+    validate(live, lane_value(ahead_pg[j], 0), lane_value(ahead_lb[j], 0),
+             MASKED ? (uint32_t)lane_value(ahead_mk[j], 0) : 0xFFFFu, page, vis);
   };
 
   auto process = [&](const PageRegs<KV> &cur, int page, uint32_t vis) {
@@ -377,18 +383,24 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   PageRegs<KV> r[RING];
   int pg[RING];
   uint32_t nv[RING];
+  // (each slot's table reads follow its page loads, as in the loop, so the
+  // wait counts at the loop header are the steady-state ones)
 #pragma unroll
   for (int j = 0; j < RING; ++j) {
-    validate(j, raw_pg[j], raw_lb[j], raw_mk[j], pg[j], nv[j]);
+    validate(j < n_my, raw_pg[j], raw_lb[j], raw_mk[j], pg[j], nv[j]);
     load_page<KV>(r[j], a, pg[j], g, lane, nv[j] != 0u);
+    __builtin_amdgcn_sched_barrier(0);
+    table_issue(u + nw * (j + RING), j);
+    __builtin_amdgcn_sched_barrier(0);
   }
   const int full = n_my - n_my % RING;
   for (int i = 0; i < full; i += RING) {
 #pragma unroll
     for (int j = 0; j < RING; ++j) {
       process(r[j], pg[j], nv[j]);
-      page_info(i + j + RING, pg[j], nv[j]);
+      page_info(i + j + RING < n_my, j, pg[j], nv[j]);
       load_page<KV>(r[j], a, pg[j], g, lane, nv[j] != 0u);
+      table_issue(u + nw * (i + j + 2 * RING), j);
     }
   }
 #pragma unroll

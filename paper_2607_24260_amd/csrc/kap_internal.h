@@ -189,6 +189,29 @@ __device__ __forceinline__ uint32_t tile_load4(__amdgpu_buffer_rsrc_t r, int off
   return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kNonTemporal);
 }
 
+// Block-table entries read ahead through the vector memory pipe. A scalar
+// load of the next entry, waited for right before the page load that needs
+// it, stalls the wavefront for a full cache round trip on every page; a
+// vector load travels in order with the KV loads, so it can be issued a ring
+// round before its use and waited for with the page data. `opaque_zero` is a
+// VGPR the compiler cannot see through (so the load stays a vector load);
+// lane l reads element idx + (l & 1) of the table row, so lanes 0 and 1 hold
+// two consecutive entries. Reads past the row's `bytes` return 0.
+__device__ __forceinline__ int opaque_zero() {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+  return z;
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t table_rsrc(const int32_t *row, int entries) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(row), 0, entries * 4, kBufDword3);
+}
+__device__ __forceinline__ int table_ahead(__amdgpu_buffer_rsrc_t r, int vzero_or_4, int idx) {
+  return (int)__builtin_amdgcn_raw_buffer_load_b32(r, vzero_or_4, idx * 4, 0);
+}
+__device__ __forceinline__ int lane_value(int v, int lane) {
+  return __builtin_amdgcn_readlane(v, lane);
+}
+
 // The (K, V) fp8 scales of a page, loaded with the page's KV data (in the
 // same in-order vector-memory stream, so they arrive with it); a dead page
 // reads nothing and gets (0, 0). Every KV head reads them, so they are

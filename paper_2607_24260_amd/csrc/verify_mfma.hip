@@ -111,14 +111,13 @@ __device__ __forceinline__ u32x4 k_operand(u32x2 x) {
 __device__ __forceinline__ u32x2 v_operand(u32x2 x) { return x; }
 __device__ __forceinline__ u32x2 v_operand(uint32_t x) { return fp8x4_to_bf16x4(x); }
 
-// Pair at pages k, k+1 (k + 1 may lie past the sequence). Missing or invalid
-// pages, and pairs past the wavefront's share (live == false), load through a
-// zero-byte descriptor: zeros, no memory traffic, and no branches.
+// Pair at pages k, k+1 (k + 1 may lie past the sequence) with physical ids
+// pa, pb (pb < 0 if there is no page k + 1). Missing or invalid pages, and
+// pairs past the wavefront's share (live == false), load through a zero-byte
+// descriptor: zeros, no memory traffic, and no branches.
 template <int KV>
-__device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, const int32_t *fbt,
-                                          int k, int k_end, int g, int n, int j, bool live) {
-  const int pa = fbt[k];
-  const int pb = (k + 1 < k_end) ? fbt[k + 1] : -1;
+__device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, int pa, int pb,
+                                          int g, int n, int j, bool live) {
   r.okA = live && pa >= 0 && (int64_t)pa < a.num_pages;
   r.okB = live && pb >= 0 && (int64_t)pb < a.num_pages;
   r.pA = r.okA ? pa : 0;
@@ -345,18 +344,31 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
     // Every round issues all RING loads unconditionally and skips only the
     // processing of pairs past the end: an early exit inside a round would
     // make the loop header wait for the just-issued loads, draining the ring
-    // every round.
+    // every round. The block-table entries of the pair a round ahead are read
+    // through the vector memory pipe (lanes 0 and 1: pages k and k + 1) right
+    // after a slot's pair loads, and used when the slot is refilled next.
     constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 ? 2 : 1);
+    const auto rt = table_rsrc(fbt, np_seq);
+    const int voff = (lane & 1) * 4;
+    auto second = [&](int k, int v) { return k + 1 < np_seq ? v : -1; };
     PairRegs<KV> rr[RING];
+    int ahead[RING];
 #pragma unroll
-    for (int jr = 0; jr < RING; ++jr)
-      load_pair<KV>(rr[jr], a, fbt, kpair(jr), np_seq, g, n, j, jr < n_my);
+    for (int jr = 0; jr < RING; ++jr) {
+      const int k = kpair(jr);
+      load_pair<KV>(rr[jr], a, fbt[k], k + 1 < np_seq ? fbt[k + 1] : -1, g, n, j, jr < n_my);
+      __builtin_amdgcn_sched_barrier(0);
+      ahead[jr] = table_ahead(rt, voff, kpair(jr + RING));
+      __builtin_amdgcn_sched_barrier(0);
+    }
     for (int i = 0; i < n_my; i += RING) {
 #pragma unroll
       for (int jr = 0; jr < RING; ++jr) {
         if (i + jr < n_my) process(rr[jr], kpair(i + jr));
-        load_pair<KV>(rr[jr], a, fbt, kpair(i + jr + RING), np_seq, g, n, j,
-                      i + jr + RING < n_my);
+        const int k = kpair(i + jr + RING);
+        load_pair<KV>(rr[jr], a, lane_value(ahead[jr], 0), second(k, lane_value(ahead[jr], 1)), g,
+                      n, j, i + jr + RING < n_my);
+        ahead[jr] = table_ahead(rt, voff, kpair(i + jr + 2 * RING));
       }
     }
   }
