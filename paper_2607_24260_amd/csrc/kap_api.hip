@@ -4,6 +4,7 @@
 #include "kap.h"
 #include "kap_diag.h"
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -89,21 +90,26 @@ struct SplitPlan {
   int n_split;    // splits per (sequence, KV head); balanced mode: workgroups launched
   int pps;        // most pages any split of the generic path can get
   int w_target;   // balanced mode: workgroups the work is spread over
+  int w_uneven;   // balanced mode, uneven batch: the same, finer chunks
   int min_chunk;  // balanced mode: fewest work items per split
   long long slots;  // tuned kernels: partial slots
 };
 
 // Balanced mode sizing: the work of a call is spread over about
-// kTargetPerCU workgroups per CU, and a split keeps at least kMinChunk* work
-// items (decode: view pages, one per wavefront and more; verify: page pairs).
-#ifndef KAP_DECODE_TARGET_PER_CU
-#define KAP_DECODE_TARGET_PER_CU 1
-#endif
-#ifndef KAP_VERIFY_TARGET_PER_CU
-#define KAP_VERIFY_TARGET_PER_CU 1
-#endif
-constexpr int kDecodeTargetPerCU = KAP_DECODE_TARGET_PER_CU;
-constexpr int kVerifyTargetPerCU = KAP_VERIFY_TARGET_PER_CU;
+// kTargetPerCU workgroups per CU (decode: per KV dtype), or over kUneven*
+// finer ones when the batch is uneven, and a split keeps at least kMinChunk*
+// work items (decode: view pages, one per wavefront and more; verify: page
+// pairs). fp8 decode takes two workgroups per CU: its widening and softmax
+// work per byte is twice bf16's, and a second workgroup on each CU hides it
+// behind the other's loads (full-context decode of 4 x 128K tokens: 186 vs
+// 201 us per call on MI355X); for bf16 the second workgroup only adds
+// requests in flight (331 vs 321 us). Uneven batches: 8 workgroups per CU
+// for decode (64 ragged fp8 sequences of 4K-128K tokens: 876 vs 974 us with
+// 4), 4 x the target for verify (8 was slower for 3-token windows).
+constexpr int kDecodeTargetPerCU[2] = {1, 2};   // bf16, fp8 KV
+constexpr int kDecodeUnevenPerCU = 8;
+constexpr int kVerifyTargetPerCU = 1;
+constexpr int kVerifyUnevenFactor = 4;
 constexpr int kMinChunkDecode = 16;
 constexpr int kMinChunkVerify = 8;
 
@@ -133,23 +139,25 @@ int blocks_per_cu(int id, int kv_type, int q_len) {
 // (sequence, KV head) units that one split each already fills the device.
 // Generic path: splits of at most kGenericPagesPerSplit pages.
 SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num_splits) {
-  SplitPlan p{fast_geometry(kv), false, 1, 1, 0, 0, 0};
+  SplitPlan p{fast_geometry(kv), false, 1, 1, 0, 0, 0, 0};
   const int mb = max_blocks > 0 ? max_blocks : 1;
   const long long units = (long long)batch * kv->num_kv_heads;
+  const int target = kDecodeTargetPerCU[kv->kv_dtype == KAP_DT_FP8_E4M3FN ? 1 : 0];
   if (p.fast) {
     if (num_splits > 0) {
       // uniform: the same split count for every (sequence, KV head)
       p.n_split = num_splits > mb ? mb : num_splits;
       p.slots = units * p.n_split;
-    } else if (units >= 4LL * kDecodeTargetPerCU * device_cus()) {
+    } else if (units >= 4LL * target * device_cus()) {
       p.n_split = 1;
       p.slots = units;
     } else {
       // balanced: split counts follow each sequence's actual view
       p.ragged = true;
-      p.w_target = kDecodeTargetPerCU * device_cus();
+      p.w_target = target * device_cus();
+      p.w_uneven = kDecodeUnevenPerCU * device_cus();
       p.min_chunk = kMinChunkDecode;
-      p.n_split = (int)((long long)kap::kUnevenFactor * p.w_target + units);
+      p.n_split = (int)((long long)std::max(p.w_target, p.w_uneven) + units);
       p.slots = p.n_split;
     }
     p.pps = cdiv(mb, p.n_split);
@@ -164,7 +172,7 @@ SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num
 
 // Verify (tuned path): as decode, with page pairs as the work items.
 SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_pages, int num_splits) {
-  SplitPlan p{fast_geometry(kv) && q_len * 4 <= 64, false, 1, 1, 0, 0, 0};
+  SplitPlan p{fast_geometry(kv) && q_len * 4 <= 64, false, 1, 1, 0, 0, 0, 0};
   const int mp = max_pages > 0 ? max_pages : 1;
   const long long units = (long long)batch * kv->num_kv_heads;
   if (p.fast) {
@@ -185,8 +193,9 @@ SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_page
       }
       p.ragged = true;
       p.w_target = kVerifyTargetPerCU * bpc * device_cus();
+      p.w_uneven = kVerifyUnevenFactor * p.w_target;
       p.min_chunk = kMinChunkVerify;
-      p.n_split = (int)((long long)kap::kUnevenFactor * p.w_target + units);
+      p.n_split = (int)((long long)p.w_uneven + units);
       p.slots = p.n_split;
     }
     p.pps = 2 * cdiv(pairs, p.n_split);
@@ -238,6 +247,7 @@ kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const Spli
   a.pages_per_split = p.pps;
   a.ragged = p.ragged ? 1 : 0;
   a.w_target = p.w_target;
+  a.w_uneven = p.w_uneven;
   a.min_chunk = p.min_chunk;
   {
     const long long units = (long long)a.batch * a.Hkv;

@@ -73,6 +73,7 @@ struct AttnArgs {
   // the partial slot. Otherwise the grid is (n_split, Hkv, batch).
   int ragged;
   int w_target;                  // balanced mode: workgroups the work is spread over
+  int w_uneven;                  // balanced mode, uneven batch: the same, finer
   int min_chunk;                 // balanced mode: fewest work items per split
   int guess_splits;              // balanced mode: max(1, w_target / (batch * Hkv))
   // Partials. Generic path: [batch * R][n_split][D] and [batch * R][n_split].
@@ -321,18 +322,18 @@ __device__ __forceinline__ int div_small(int n, int d) {
 // view pages; verify: page pairs), counted up to 2^24 for sizing. With
 // T = Hkv * sum_b items_b, the chunk is C = max(min_chunk, T / w_target)
 // items when the sequences are even (the largest holds at most 5/4 of the
-// mean: one split per workgroup slot is then balanced), else
-// T / (kUnevenFactor * w_target) -- finer chunks, which the hardware
-// dispatcher spreads over the CUs as they free up. Every (b, g) gets
-// n_b = max(1, round(items_b / C)) splits; slots are numbered sequence-major,
-// then KV head, then split. Workgroup w takes slot w and returns false past
-// the last slot. The result is the same in every wavefront, which computes
-// it alone (two passes over the batch, 64 sequences per pass). The grid
-// needs kUnevenFactor * w_target + batch * Hkv workgroups at most.
-#ifndef KAP_UNEVEN_FACTOR
-#define KAP_UNEVEN_FACTOR 4
-#endif
-constexpr int kUnevenFactor = KAP_UNEVEN_FACTOR;
+// mean: one split per workgroup slot is then balanced), else T / w_uneven --
+// finer chunks, which the hardware dispatcher spreads over the CUs as they
+// free up. Every (b, g) gets n_b = max(1, round(items_b / C)) splits when
+// the batch is even -- for equal views exactly w_target / (batch * Hkv), one
+// workgroup per slot -- and max(1, ceil(items_b / C)) when it is uneven, so
+// that no split holds more than C items (rounding to nearest there left
+// splits of up to 1.5 C, and the call waited for them at its end). Slots are
+// numbered sequence-major, then KV head, then split. Workgroup w takes slot w
+// and returns false past the last slot. The result is the same in every
+// wavefront, which computes it alone (two passes over the batch, 64
+// sequences per pass). Since C >= T / W, the slots number at most
+// W + batch * Hkv, W = max(w_target, w_uneven): the grid the host launches.
 constexpr int kMapItemCap = 1 << 24;
 
 // What the map reads per sequence: its work items and one more value the
@@ -365,7 +366,7 @@ __device__ __forceinline__ bool ragged_map(const AttnArgs &a, Load load, const S
   }
   const long long T = tot * a.Hkv;
   const bool even = 4LL * mx * a.batch <= 5 * tot;
-  const int W = even ? a.w_target : kUnevenFactor * a.w_target;
+  const int W = even ? a.w_target : a.w_uneven;
   // C = ceil(T / W) through a correctly rounded double quotient: it can come
   // out below the exact ceiling only by less than W * 2^-52 slots' worth,
   // which cannot lift the slot count past W + batch * Hkv
@@ -379,7 +380,7 @@ __device__ __forceinline__ bool ragged_map(const AttnArgs &a, Load load, const S
     SeqLoad m = first;
     if (b0 > 0) m = in ? load(b) : SeqLoad{0, 0};
     const int v = min(m.items, kMapItemCap);
-    const int nb = in ? max(1, div_small(v + Ci / 2, Ci)) : 0;
+    const int nb = in ? max(1, div_small(v + (even ? Ci / 2 : Ci - 1), Ci)) : 0;
     const int cnt = nb * a.Hkv;
     const int incl = wave_scan_add(cnt);
     const int excl = incl - cnt;
