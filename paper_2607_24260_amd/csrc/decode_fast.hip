@@ -10,20 +10,27 @@
 // last for its (sequence, KV head) merges all splits (atomic arrival counter
 // in the workspace), so one launch produces the final output.
 //
-// Per page (16 tokens x 128 dims = 4 KB of bf16 K and 4 KB of V^T):
-//  * K phase: lane (t = lane/4, c = lane%4) loads dims {32i + 8c .. +7}, i<4,
-//    of token t: four 16-byte loads, and since K pages are stored in 8-dim
-//    chunks ([chunk][token][8]) each instruction reads 1 KB contiguously. It
-//    forms partial dot products for the four query heads with v_dot2_f32_bf16. A transposing reduction inside each
-//    lane quad leaves lane (t, c) holding the full logit of token t, head c.
-//  * softmax: page maxima per head come from row rotations plus permlane16 /
-//    permlane32 swaps; the running max, rescale factor and sum are kept per
-//    head in every lane that owns that head.
-//  * V phase: the V^T page is read as four contiguous 1 KB rows of 16-byte
-//    loads; lane owns dims {32i + lane/2} for tokens 8*(lane%2) .. +7, takes
-//    the probabilities of those tokens from LDS and accumulates o in fp32.
-// Everything is memory-bound: 4 flop per KV byte against a VALU ridge of
-// ~20 flop/byte, so no matrix cores are used here.
+// Both products of a page run on the matrix cores with the 4x4x4 bf16
+// instruction (16 independent 4x4 blocks per wavefront), whose 4-row blocks
+// fit the four query heads of a KV head. Lane l = 16 tg + 4 dg + j:
+//  * logits: block (tg, dg) multiplies the four heads' query slice of dims
+//    32 dg .. 32 dg + 31 with token 4 tg + j's K slice, 4 dims per step, 8
+//    steps. K pages are stored in 8-dim chunks ([chunk][token][8]), so a lane
+//    reads four chunks of its token and each load instruction reads four full
+//    chunk rows (4 x 128 / 256 bytes). Row rotations sum the four dim groups;
+//    lane l then keeps the logit of head dg, token 4 tg + j.
+//  * softmax: page maxima per head over lane bits 0-1 (quad swaps) and 4-5
+//    (permlane16 / permlane32 swaps); running max and sum per head in every
+//    lane that owns that head.
+//  * o += p V: every block multiplies the four heads' weights of 4 tokens with
+//    the V values of 4 dims; lane l reads V^T rows l and l + 64 (1 KB
+//    contiguous per load instruction for fp8) and accumulates o for the four
+//    heads at dims l and l + 64. The weights travel through LDS as bf16
+//    hi + lo parts (error below 2^-15 relative), so the matrix product keeps
+//    near-fp32 weights.
+// fp8 KV is widened to bf16 at use (exact); per-page scales fold into the
+// logit scale and the weights. Moving the 4 flop per KV byte off the vector
+// ALU leaves it the widening and the softmax, and the loads set the pace.
 #include "kap_internal.h"
 
 namespace kap {
@@ -31,7 +38,8 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kD = 128;
 constexpr int kWaves = 4;
@@ -48,9 +56,12 @@ constexpr int kWaves = 4;
 constexpr int kRingBF16 = KAP_DECODE_RING_BF16;
 constexpr int kRingFP8 = KAP_DECODE_RING_FP8;
 
-__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a),
-                                         __builtin_bit_cast(bf16x2, b), c, false);
+// D += A B on 16 blocks of 4x4 (K = 4, bf16 operands, fp32 accumulation):
+// block b = lane / 4; A row i of block b comes from lane 4 b + i, B column j
+// from lane 4 b + j, and D[i][j] lands in element i of lane 4 b + j.
+__device__ __forceinline__ f32x4 mfma4(u32x2 a, u32x2 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(__builtin_bit_cast(s16x4, a),
+                                                 __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
 }
 
 template <int CTRL>
@@ -79,10 +90,11 @@ __device__ __forceinline__ float xor32_sum(float x) {
   return __int_as_float(r[0]) + __int_as_float(r[1]);
 }
 
-// Raw registers of one page: K slice and V^T slice of this lane.
+// Raw registers of one page. k[cc]: chunk 4 dg + cc (dims 32 dg + 8 cc ..
+// + 7) of token 4 tg + j; v: V^T rows l and l + 64 (16 tokens each).
 template <int KV> struct PageRegs;
-template <> struct PageRegs<kBF16> { u32x4 k[4]; u32x4 v[4]; };
-template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x2 v[4]; float2 sc; };   // sc: (K, V) scales
+template <> struct PageRegs<kBF16> { u32x4 k[4]; u32x4 v[4]; };   // v[0..1]: row l, v[2..3]: row l + 64
+template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x4 v[2]; float2 sc; };   // sc: (K, V) scales
 
 // Loads of one (page, head) tile. With live == false the descriptor covers
 // zero bytes: the loads return zeros without touching memory (used for
@@ -90,74 +102,84 @@ template <> struct PageRegs<kFP8> { u32x2 k[4]; u32x2 v[4]; float2 sc; };   // s
 template <int KV>
 __device__ __forceinline__ void load_page(PageRegs<KV> &r, const AttnArgs &a, int page, int g,
                                           int lane, bool live) {
-  const int t = lane >> 2, c = lane & 3;
+  const int t = ((lane >> 4) << 2) | (lane & 3), dg = (lane >> 2) & 3;
   constexpr int kTile = (KV == kBF16 ? 2 : 1) * kPage * kD;   // bytes per (page, head) tile
   const size_t off = ((size_t)page * a.Hkv + g) * kTile;
   const int bytes = live ? kTile : 0;
   const auto kr = tile_rsrc(a.k_pages, off, bytes);
   const auto vr = tile_rsrc(a.v_pages, off, bytes);
   if constexpr (KV == kBF16) {
-    // K: chunk 4i + c of token t; V^T: 1 KB row block i, 16 bytes per lane
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r.k[i] = tile_load16(kr, i * 1024 + c * 256 + t * 16);
+    for (int cc = 0; cc < 4; ++cc) r.k[cc] = tile_load16(kr, (4 * dg + cc) * 256 + t * 16);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r.v[i] = tile_load16(vr, i * 1024 + lane * 16);
+    for (int h = 0; h < 2; ++h) {
+      r.v[2 * h] = tile_load16(vr, (64 * h + lane) * 32);
+      r.v[2 * h + 1] = tile_load16(vr, (64 * h + lane) * 32 + 16);
+    }
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r.k[i] = tile_load8(kr, i * 512 + c * 128 + t * 8);
+    for (int cc = 0; cc < 4; ++cc) r.k[cc] = tile_load8(kr, (4 * dg + cc) * 128 + t * 8);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) r.v[i] = tile_load8(vr, i * 512 + lane * 8);
+    for (int h = 0; h < 2; ++h) r.v[h] = tile_load16(vr, (64 * h + lane) * 16);
     r.sc = page_scales(a.kv_scales, page, live);
   }
 }
 
-// K slice of this lane as bf16 pairs: kk[i][w] holds dims 32i + 8c + 2w, +1.
+// K operand of logit step st (dims 32 dg + 4 st .. + 3 of this lane's token)
+// as four bf16 values.
 template <int KV>
-__device__ __forceinline__ void k_pairs(const PageRegs<KV> &r, uint32_t kk[4][4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if constexpr (KV == kBF16) {
-#pragma unroll
-      for (int w = 0; w < 4; ++w) kk[i][w] = r.k[i][w];
-    } else {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const kv_u32x2 w = fp8x4_to_bf16x4(r.k[i][h]);
-        kk[i][2 * h] = w[0];
-        kk[i][2 * h + 1] = w[1];
-      }
-    }
+__device__ __forceinline__ u32x2 k_operand(const PageRegs<KV> &r, int st) {
+  const int cc = st >> 1, h = st & 1;
+  if constexpr (KV == kBF16)
+    return u32x2{r.k[cc][2 * h], r.k[cc][2 * h + 1]};
+  else
+    return fp8x4_to_bf16x4(r.k[cc][h]);
+}
+
+// V operand of weight step st (tokens 4 st .. 4 st + 3 of V^T row
+// 64 half + l) as four bf16 values, after the page's visibility masks were
+// applied to the raw registers.
+template <int KV>
+__device__ __forceinline__ u32x2 v_operand(const PageRegs<KV> &r, int half, int st) {
+  if constexpr (KV == kBF16) {
+    const u32x4 &w = r.v[2 * half + (st >> 1)];
+    return (st & 1) ? u32x2{w[2], w[3]} : u32x2{w[0], w[1]};
+  } else {
+    return fp8x4_to_bf16x4(r.v[half][st]);
   }
 }
 
-// V^T slice as floats: vv[i][j] = V[token 8*(lane%2) + j][dim 32i + lane/2].
+// Clears the V values of tokens whose bit in vis is 0, so that their zero
+// weights meet zeros (not whatever the page holds there). vis is the same in
+// every lane, so the byte / half-word masks are scalar work.
 template <int KV>
-__device__ __forceinline__ void v_floats(const PageRegs<KV> &r, float vv[4][8]) {
+__device__ __forceinline__ void mask_v(PageRegs<KV> &r, uint32_t vis) {
+  if constexpr (KV == kBF16) {
+    // dword w of a row holds tokens 2 w, 2 w + 1 (w = 0..7 over v[2h], v[2h+1])
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if constexpr (KV == kBF16) {
+    for (int w = 0; w < 8; ++w) {
+      const uint32_t m = ((vis >> (2 * w)) & 1u ? 0x0000FFFFu : 0u) |
+                         ((vis >> (2 * w + 1)) & 1u ? 0xFFFF0000u : 0u);
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        vv[i][2 * w] = bf16_lo(r.v[i][w]);
-        vv[i][2 * w + 1] = bf16_hi(r.v[i][w]);
-      }
-    } else {
+      for (int h = 0; h < 2; ++h) r.v[2 * h + (w >> 2)][w & 3] &= m;
+    }
+  } else {
+    // dword w of a row holds tokens 4 w .. 4 w + 3, one byte each
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const float2 f0 = fp8x2_to_f32<false>(r.v[i][h]);
-        const float2 f1 = fp8x2_to_f32<true>(r.v[i][h]);
-        vv[i][4 * h + 0] = f0.x;
-        vv[i][4 * h + 1] = f0.y;
-        vv[i][4 * h + 2] = f1.x;
-        vv[i][4 * h + 3] = f1.y;
-      }
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t nib = (vis >> (4 * w)) & 0xFu;
+      const uint32_t m = ((nib & 1u) ? 0x000000FFu : 0u) | ((nib & 2u) ? 0x0000FF00u : 0u) |
+                         ((nib & 4u) ? 0x00FF0000u : 0u) | ((nib & 8u) ? 0xFF000000u : 0u);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) r.v[h][w] &= m;
     }
   }
 }
 
 template <int KV, int RING, bool BALANCED, bool MASKED>
 __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
-  __shared__ float pbuf[kWaves][64];
+  __shared__ __attribute__((aligned(16))) uint16_t pw_hi[kWaves][4][kPage];   // weights (x V scale), bf16 hi + lo
+  __shared__ __attribute__((aligned(16))) uint16_t pw_lo[kWaves][4][kPage];
   __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
   __shared__ float wacc[kWaves][4][kD];
   __shared__ float s_part[4][kD];
@@ -166,7 +188,9 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  const int t = lane >> 2, c = lane & 3, hf = lane & 1;
+  // lane roles: logits of token t = 4 tg + j, dim group / owned head dg;
+  // weight rows: head hq; output columns: dims lane and lane + 64
+  const int t = ((lane >> 4) << 2) | (lane & 3), dg = (lane >> 2) & 3, hq = lane & 3;
 
   // Work unit. Balanced mode: the map needs the view lengths of the whole
   // batch, so the first table entries are read for a guess while it is
@@ -249,27 +273,23 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     ahead_mk[j] = MASKED ? table_ahead(rmk, vz, kk) : 0xFFFF;
   };
 
-  // query slices of the four heads, as bf16 pairs matching the K slice
-  uint32_t qr[4][4][4];
+  // query operand of logit step st: head hq, dims 32 dg + 4 st .. + 3 (bf16)
+  u32x2 qa[8];
   {
-    const uint16_t *qb = static_cast<const uint16_t *>(a.q) + ((size_t)b * a.Hq + g * 4) * kD;
+    const uint16_t *qb =
+        static_cast<const uint16_t *>(a.q) + ((size_t)b * a.Hq + g * 4 + hq) * kD + 32 * dg;
 #pragma unroll
-    for (int hh = 0; hh < 4; ++hh)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4 v = *reinterpret_cast<const u32x4 *>(qb + hh * kD + i * 32 + c * 8);
-#pragma unroll
-        for (int w = 0; w < 4; ++w) qr[hh][i][w] = v[w];
-      }
+    for (int q4 = 0; q4 < 4; ++q4) {
+      const u32x4 v = *reinterpret_cast<const u32x4 *>(qb + 8 * q4);
+      qa[2 * q4] = u32x2{v[0], v[1]};
+      qa[2 * q4 + 1] = u32x2{v[2], v[3]};
+    }
   }
 
-  float m_c = -INFINITY;     // running max (log2 units) of head c
-  float l_c = 0.f;           // partial sum of p over this lane's tokens, head c
-  float acc[4][4];           // [head][dim i] over this lane's token half
-#pragma unroll
-  for (int hh = 0; hh < 4; ++hh)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) acc[hh][i] = 0.f;
+  float m_c = -INFINITY;     // running max (log2 units) of head dg
+  float l_c = 0.f;           // partial sum of p over this lane's tokens, head dg
+  f32x4 o_lo = {0.f, 0.f, 0.f, 0.f};   // o[head i][dim lane]
+  f32x4 o_hi = {0.f, 0.f, 0.f, 0.f};   // o[head i][dim lane + 64]
 
   const int n_my = u < nb ? div_small(nb - 1 - u, nw) + 1 : 0;
 
@@ -294,82 +314,73 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
              MASKED ? (uint32_t)lane_value(ahead_mk[j], 0) : 0xFFFFu, page, vis);
   };
 
-  auto process = [&](const PageRegs<KV> &cur, int page, uint32_t vis) {
+  auto process = [&](PageRegs<KV> &cur, int page, uint32_t vis) {
     float ksc = a.scale_log2, vsc = 1.f;
     if constexpr (KV == kFP8) {
       ksc *= cur.sc.x;
       vsc = cur.sc.y;
     }
-    // ---- logits --------------------------------------------------------------
-    uint32_t kk[4][4];
-    k_pairs<KV>(cur, kk);
-    float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
+    // ---- logits: partial over this lane's dim group, then summed ---------------
+    f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int st = 0; st < 8; st += 2) {
+      sa = mfma4(qa[st], k_operand<KV>(cur, st), sa);
+      sb = mfma4(qa[st + 1], k_operand<KV>(cur, st + 1), sb);
+    }
+    f32x4 sc4 = sa + sb;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        d0 = dot2(kk[i][w], qr[0][i][w], d0);
-        d1 = dot2(kk[i][w], qr[1][i][w], d1);
-        d2 = dot2(kk[i][w], qr[2][i][w], d2);
-        d3 = dot2(kk[i][w], qr[3][i][w], d3);
-      }
-    // transposing reduction inside the quad: lane c ends with head c
-    const bool o1 = c & 1, o2 = c & 2;
-    float keep0 = o1 ? d1 : d0, send0 = o1 ? d0 : d1;
-    float keep1 = o1 ? d3 : d2, send1 = o1 ? d2 : d3;
-    keep0 += dpp<kQuadXor1>(send0);
-    keep1 += dpp<kQuadXor1>(send1);
-    float s = o2 ? keep1 : keep0;
-    s += dpp<kQuadXor2>(o2 ? keep0 : keep1);
+    for (int i = 0; i < 4; ++i) {
+      sc4[i] += dpp<kRowRor4>(sc4[i]);
+      sc4[i] += dpp<kRowRor8>(sc4[i]);
+    }
+    float s = dg == 0 ? sc4[0] : dg == 1 ? sc4[1] : dg == 2 ? sc4[2] : sc4[3];
     s = ((vis >> t) & 1u) ? s * ksc : -INFINITY;
 
     // ---- online softmax ------------------------------------------------------
-    float pm = fmaxf(s, dpp<kRowRor4>(s));
-    pm = fmaxf(pm, dpp<kRowRor8>(pm));
+    float pm = fmaxf(s, dpp<kQuadXor1>(s));
+    pm = fmaxf(pm, dpp<kQuadXor2>(pm));
     pm = xor16_max(pm);
     pm = xor32_max(pm);
     const float m_new = fmaxf(m_c, pm);
     if (__any(m_new > m_c)) {
       const float alpha = exp2_fast(m_c - (m_new == -INFINITY ? 0.f : m_new));
       l_c *= alpha;
-      float al[4];
 #pragma unroll
-      for (int hh = 0; hh < 4; ++hh)
-        al[hh] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), hh));
-#pragma unroll
-      for (int hh = 0; hh < 4; ++hh)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[hh][i] *= al[hh];
+      for (int hh = 0; hh < 4; ++hh) {
+        // lane 4 hh owns head hh
+        const float al = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), 4 * hh));
+        o_lo[hh] *= al;
+        o_hi[hh] *= al;
+      }
       m_c = m_new;
     }
     const float p = exp2_fast(s - (m_c == -INFINITY ? 0.f : m_c));
     l_c += p;
-    pbuf[wave][lane] = p * vsc;
+    const float pv = p * vsc;
+    const uint32_t hi = __float_as_uint(pv) & 0xFFFF0000u;
+    pw_hi[wave][dg][t] = (uint16_t)(hi >> 16);
+    pw_lo[wave][dg][t] = (uint16_t)(__float_as_uint(pv - __uint_as_float(hi)) >> 16);
+    if (vis != 0xFFFFu) mask_v<KV>(cur, vis);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
     // ---- o += p V --------------------------------------------------------------
-    float vv[4][8];
-    v_floats<KV>(cur, vv);
-    if (vis != 0xFFFFu) {
+    const u32x4 ph0 = *reinterpret_cast<const u32x4 *>(&pw_hi[wave][hq][0]);
+    const u32x4 ph1 = *reinterpret_cast<const u32x4 *>(&pw_hi[wave][hq][8]);
+    const u32x4 pl0 = *reinterpret_cast<const u32x4 *>(&pw_lo[wave][hq][0]);
+    const u32x4 pl1 = *reinterpret_cast<const u32x4 *>(&pw_lo[wave][hq][8]);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const bool ok = (vis >> (hf * 8 + j)) & 1u;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) vv[i][j] = ok ? vv[i][j] : 0.f;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float4 pj = *reinterpret_cast<const float4 *>(&pbuf[wave][(hf * 8 + j) * 4]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[0][i] = fmaf(pj.x, vv[i][j], acc[0][i]);
-        acc[1][i] = fmaf(pj.y, vv[i][j], acc[1][i]);
-        acc[2][i] = fmaf(pj.z, vv[i][j], acc[2][i]);
-        acc[3][i] = fmaf(pj.w, vv[i][j], acc[3][i]);
-      }
+    for (int st = 0; st < 4; ++st) {
+      const u32x4 &h4 = st < 2 ? ph0 : ph1;
+      const u32x4 &l4 = st < 2 ? pl0 : pl1;
+      const u32x2 ah = (st & 1) ? u32x2{h4[2], h4[3]} : u32x2{h4[0], h4[1]};
+      const u32x2 al = (st & 1) ? u32x2{l4[2], l4[3]} : u32x2{l4[0], l4[1]};
+      const u32x2 v0 = v_operand<KV>(cur, 0, st), v1 = v_operand<KV>(cur, 1, st);
+      o_lo = mfma4(ah, v0, o_lo);
+      o_hi = mfma4(ah, v1, o_hi);
+      o_lo = mfma4(al, v0, o_lo);
+      o_hi = mfma4(al, v1, o_hi);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -411,23 +422,18 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     if (full + j < n_my) process(r[j], pg[j], nv[j]);
 
   // ---- per-wave totals -------------------------------------------------------
-  float lt = l_c + dpp<kRowRor4>(l_c);
-  lt += dpp<kRowRor8>(lt);
+  float lt = l_c + dpp<kQuadXor1>(l_c);
+  lt += dpp<kQuadXor2>(lt);
   lt = xor16_sum(lt);
   lt = xor32_sum(lt);
-#pragma unroll
-  for (int hh = 0; hh < 4; ++hh)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) acc[hh][i] += dpp<kQuadXor1>(acc[hh][i]);
-  if (lane < 4) {
-    wstat[0][wave][lane] = m_c;
-    wstat[1][wave][lane] = lt;
+  if ((lane & 0x33) == 0) {   // lanes 0, 4, 8, 12: heads 0..3
+    wstat[0][wave][dg] = m_c;
+    wstat[1][wave][dg] = lt;
   }
-  if (hf == 0) {
 #pragma unroll
-    for (int hh = 0; hh < 4; ++hh)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) wacc[wave][hh][i * 32 + (lane >> 1)] = acc[hh][i];
+  for (int hh = 0; hh < 4; ++hh) {
+    wacc[wave][hh][lane] = o_lo[hh];
+    wacc[wave][hh][64 + lane] = o_hi[hh];
   }
   __syncthreads();
 

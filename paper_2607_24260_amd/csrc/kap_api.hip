@@ -99,13 +99,13 @@ struct SplitPlan {
 // kTargetPerCU workgroups per CU (decode: per KV dtype), or over kUneven*
 // finer ones when the batch is uneven, and a split keeps at least kMinChunk*
 // work items (decode: view pages, one per wavefront and more; verify: page
-// pairs). fp8 decode takes two workgroups per CU: its widening and softmax
-// work per byte is twice bf16's, and a second workgroup on each CU hides it
-// behind the other's loads (full-context decode of 4 x 128K tokens: 186 vs
-// 201 us per call on MI355X); for bf16 the second workgroup only adds
-// requests in flight (331 vs 321 us). Uneven batches: 8 workgroups per CU
-// for decode (64 ragged fp8 sequences of 4K-128K tokens: 876 vs 974 us with
-// 4), 4 x the target for verify (8 was slower for 3-token windows).
+// pairs). fp8 decode takes two workgroups per CU: its widening work per
+// byte is twice bf16's, and a second workgroup on each CU hides it behind
+// the other's loads (full-context decode of 4 x 128K tokens on MI355X: 167.8
+// vs 170.0 us per call); for bf16 the second workgroup only adds requests in
+// flight. Uneven batches: 8 workgroups per CU for decode (64 ragged fp8
+// sequences of 4K-128K tokens: 772 vs 795 us with 4), 4 x the target for
+// verify (8 was slower for 3-token windows).
 constexpr int kDecodeTargetPerCU[2] = {1, 2};   // bf16, fp8 KV
 constexpr int kDecodeUnevenPerCU = 8;
 constexpr int kVerifyTargetPerCU = 1;
