@@ -149,8 +149,20 @@ constexpr int kVerifyWaves = 4;
 // fewer spills; fp8 pairs are half the bytes of bf16 pairs)
 constexpr int kRingFP8Small = 2;
 
+// Wavefronts per SIMD the compiler must leave room for. fp8 windows of 5-12
+// tokens (two or three row tiles) are issue-bound at one wavefront per SIMD:
+// their widening and softmax instructions wait behind their own matrix
+// products. Widening at use (and, with three tiles, one page pair in flight
+// per wavefront) keeps them within 256 registers, so a second wavefront per
+// SIMD fits without spills and overlaps the two (ragged fp8 verify on MI355X:
+// 5-token windows 1014 vs 1114 us, 9-token windows 1254 vs 1374 us). bf16
+// kernels and fp8 with four tiles would spill; fp8 with one tile already
+// runs two per SIMD (asking for it explicitly cost 1%).
+constexpr int verify_min_waves(int kv, int nt) { return kv == kFP8 && (nt == 2 || nt == 3) ? 2 : 1; }
+
 template <int KV, int NT>
-__global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(verify_min_waves(KV, NT))))
+void verify_mfma_kernel(AttnArgs a) {
   __shared__ float s_acc[kVerifyWaves][16][kD + 4];
   __shared__ float s_m[kVerifyWaves][16];
   __shared__ float s_l[kVerifyWaves][16];
@@ -220,7 +232,8 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  // RING pair buffers (three, two for fp8; two for 9..12-token windows, one beyond),
+  // RING pair buffers (three, two for fp8; bf16 9..12-token windows two; fp8
+  // 9..12-token windows and 13..16-token windows one),
   // unrolled: while one pair is processed the loads of the next ones are in
   // flight. Past the end of this wavefront's pairs the loads go through an
   // empty descriptor (no traffic), so the steady state is straight-line code.
@@ -233,45 +246,42 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
       kscB *= P.scB.x;
       vscB = P.scB.y;
     }
-    u32x2 vA[8], vB[8];   // V^T operand halves as bf16
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      vA[dt] = v_operand(P.vA[dt]);
-      vB[dt] = v_operand(P.vB[dt]);
-    }
-
-    // keys at or beyond L hold no data: zero their V so 0 * garbage cannot occur
+    // keys at or beyond L hold no data: zero their V so 0 * garbage cannot
+    // occur (on the raw registers: bytes of fp8 codes, halves of bf16 pairs)
     if ((k + 2) * kPage > L) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const bool zA = k * kPage + 4 * j + e >= L;
         const bool zB = (k + 1) * kPage + 4 * j + e >= L;
-        const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          if (zA) vA[dt][e >> 1] &= mask;
-          if (zB) vB[dt][e >> 1] &= mask;
+          if constexpr (KV == kFP8) {
+            const uint32_t mask = ~(0xFFu << (8 * e));
+            if (zA) P.vA[dt] &= mask;
+            if (zB) P.vB[dt] &= mask;
+          } else {
+            const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
+            if (zA) P.vA[dt][e >> 1] &= mask;
+            if (zB) P.vB[dt][e >> 1] &= mask;
+          }
         }
       }
     }
 
-    u32x4 kA[4], kB[4];   // K operands as bf16
-#pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      kA[kb] = k_operand(P.kA[kb]);
-      kB[kb] = k_operand(P.kB[kb]);
-    }
-
-    // ---- S^T = K Q^T ------------------------------------------------------------
+    // ---- S^T = K Q^T (K operands widened at use) ---------------------------------
     f32x4 sA[NT], sB[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       sA[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
       sB[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        sA[nt] = mfma(kA[kb], qop[nt][kb], sA[nt]);
-        sB[nt] = mfma(kB[kb], qop[nt][kb], sB[nt]);
+    for (int kb = 0; kb < 4; ++kb) {
+      const u32x4 kA = k_operand(P.kA[kb]), kB = k_operand(P.kB[kb]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        sA[nt] = mfma(kA, qop[nt][kb], sA[nt]);
+        sB[nt] = mfma(kB, qop[nt][kb], sB[nt]);
       }
     }
 
@@ -328,7 +338,8 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
     // ---- O^T += V^T P^T -----------------------------------------------------------
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const u32x4 vop = u32x4{vA[dt][0], vA[dt][1], vB[dt][0], vB[dt][1]};
+      const u32x2 va = v_operand(P.vA[dt]), vb = v_operand(P.vB[dt]);
+      const u32x4 vop = u32x4{va[0], va[1], vb[0], vb[1]};
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         acc[nt][dt] = mfma(vop, phi[nt], acc[nt][dt]);
@@ -347,7 +358,7 @@ __global__ __launch_bounds__(256) void verify_mfma_kernel(AttnArgs a) {
     // every round. The block-table entries of the pair a round ahead are read
     // through the vector memory pipe (lanes 0 and 1: pages k and k + 1) right
     // after a slot's pair loads, and used when the slot is refilled next.
-    constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 ? 2 : 1);
+    constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 && KV == kBF16 ? 2 : 1);
     const auto rt = table_rsrc(fbt, np_seq);
     const int voff = (lane & 1) * 4;
     auto second = [&](int k, int v) { return k + 1 < np_seq ? v : -1; };
