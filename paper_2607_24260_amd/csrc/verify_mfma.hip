@@ -27,6 +27,8 @@
 // The four wavefronts combine through LDS; with several splits, the workgroup
 // that finishes last for its (sequence, KV head) merges all splits (atomic
 // arrival counter in the workspace), so one launch produces the final output.
+#include <type_traits>
+
 #include "kap_internal.h"
 
 namespace kap {
@@ -77,7 +79,7 @@ template <> struct PairData<kBF16> {
 };
 template <> struct PairData<kFP8> {
   u32x2 kA[4], kB[4];   // the same elements as fp8 codes
-  uint32_t vA[8], vB[8];
+  u32x4 vA[2], vB[2];   // V^T rows 64 c + lane (all 16 keys), rearranged at use (vt_tiles)
   float2 scA, scB;      // (K, V) scales of the two pages
 };
 template <int KV>
@@ -98,10 +100,6 @@ __device__ __forceinline__ u32x2 load_k(__amdgpu_buffer_rsrc_t r, int n, int j, 
 __device__ __forceinline__ u32x2 load_vt(__amdgpu_buffer_rsrc_t r, int n, int j, int dt, u32x2) {
   return tile_load8(r, dt * 512 + n * 32 + j * 8);
 }
-__device__ __forceinline__ uint32_t load_vt(__amdgpu_buffer_rsrc_t r, int n, int j, int dt,
-                                            uint32_t) {
-  return tile_load4(r, dt * 256 + n * 16 + j * 4);
-}
 // ... and as bf16 operands
 __device__ __forceinline__ u32x4 k_operand(u32x4 x) { return x; }
 __device__ __forceinline__ u32x4 k_operand(u32x2 x) {
@@ -110,6 +108,39 @@ __device__ __forceinline__ u32x4 k_operand(u32x2 x) {
 }
 __device__ __forceinline__ u32x2 v_operand(u32x2 x) { return x; }
 __device__ __forceinline__ u32x2 v_operand(uint32_t x) { return fp8x4_to_bf16x4(x); }
+
+// fp8 V^T: the operand piece of lane (j, n) -- keys 4j .. 4j+3 of dim 16 dt + n
+// -- is 4 bytes, and loading it directly puts lane 16 j + n at byte 16 n + 4 j:
+// neighbouring lanes 16 bytes apart, which read at ~5.4-5.9 TB/s against ~6.8
+// for the same bytes as whole rows (random-page read probes on MI355X). So each
+// lane loads whole rows 64 c + lane (16 keys = 4 dwords) and the pieces are
+// moved into place at use: row j of the wavefront holds dword w of tile
+// 4 c + j and needs dword j of tiles 4 c .. 4 c + 3, a 4 x 4 dword transpose
+// across the four 16-lane rows done by two rounds of row swaps.
+__device__ __forceinline__ void swap_rows16(uint32_t &a, uint32_t &b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(a, b, false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ void swap_rows32(uint32_t &a, uint32_t &b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(a, b, false, false);
+  a = r[0];
+  b = r[1];
+}
+__device__ __forceinline__ void vt_tiles(const u32x4 rows[2], uint32_t out[8]) {
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    uint32_t r0 = rows[c][0], r1 = rows[c][1], r2 = rows[c][2], r3 = rows[c][3];
+    swap_rows16(r0, r1);
+    swap_rows16(r2, r3);
+    swap_rows32(r0, r2);
+    swap_rows32(r1, r3);
+    out[4 * c + 0] = r0;
+    out[4 * c + 1] = r1;
+    out[4 * c + 2] = r2;
+    out[4 * c + 3] = r3;
+  }
+}
 
 // Pair at pages k, k+1 (k + 1 may lie past the sequence) with physical ids
 // pa, pb (pb < 0 if there is no page k + 1). Missing or invalid pages, and
@@ -133,10 +164,18 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, in
     r.kA[kb] = load_k(kra, n, j, kb, r.kA[kb]);
     r.kB[kb] = load_k(krb, n, j, kb, r.kB[kb]);
   }
+  if constexpr (KV == kBF16) {
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    r.vA[dt] = load_vt(vra, n, j, dt, r.vA[dt]);
-    r.vB[dt] = load_vt(vrb, n, j, dt, r.vB[dt]);
+    for (int dt = 0; dt < 8; ++dt) {
+      r.vA[dt] = load_vt(vra, n, j, dt, r.vA[dt]);
+      r.vB[dt] = load_vt(vrb, n, j, dt, r.vB[dt]);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      r.vA[c] = tile_load16(vra, c * 1024 + (16 * j + n) * 16);
+      r.vB[c] = tile_load16(vrb, c * 1024 + (16 * j + n) * 16);
+    }
   }
   if constexpr (KV == kFP8) {
     r.scA = page_scales(a.kv_scales, r.pA, r.okA);
@@ -246,6 +285,19 @@ void verify_mfma_kernel(AttnArgs a) {
       kscB *= P.scB.x;
       vscB = P.scB.y;
     }
+    // V^T pieces of lane (j, n): keys 4j .. 4j+3 of dims 16 dt + n, raw
+    using VPiece = typename std::conditional<KV == kBF16, u32x2, uint32_t>::type;
+    VPiece vA[8], vB[8];
+    if constexpr (KV == kBF16) {
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        vA[dt] = P.vA[dt];
+        vB[dt] = P.vB[dt];
+      }
+    } else {
+      vt_tiles(P.vA, vA);
+      vt_tiles(P.vB, vB);
+    }
     // keys at or beyond L hold no data: zero their V so 0 * garbage cannot
     // occur (on the raw registers: bytes of fp8 codes, halves of bf16 pairs)
     if ((k + 2) * kPage > L) {
@@ -257,12 +309,12 @@ void verify_mfma_kernel(AttnArgs a) {
         for (int dt = 0; dt < 8; ++dt) {
           if constexpr (KV == kFP8) {
             const uint32_t mask = ~(0xFFu << (8 * e));
-            if (zA) P.vA[dt] &= mask;
-            if (zB) P.vB[dt] &= mask;
+            if (zA) vA[dt] &= mask;
+            if (zB) vB[dt] &= mask;
           } else {
             const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
-            if (zA) P.vA[dt][e >> 1] &= mask;
-            if (zB) P.vB[dt][e >> 1] &= mask;
+            if (zA) vA[dt][e >> 1] &= mask;
+            if (zB) vB[dt][e >> 1] &= mask;
           }
         }
       }
@@ -338,7 +390,7 @@ void verify_mfma_kernel(AttnArgs a) {
     // ---- O^T += V^T P^T -----------------------------------------------------------
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const u32x2 va = v_operand(P.vA[dt]), vb = v_operand(P.vB[dt]);
+      const u32x2 va = v_operand(vA[dt]), vb = v_operand(vB[dt]);
       const u32x4 vop = u32x4{va[0], va[1], vb[0], vb[1]};
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
