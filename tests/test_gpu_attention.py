@@ -259,6 +259,23 @@ def test_verify_window_sizes_ragged(q_len):
     assert_close("LSE", lse.cpu().numpy(), el, LSE_TOL)
 
 
+@pytest.mark.parametrize("q_len", [1, 2, 3, 5, 8, 9, 12, 13, 16])
+def test_verify_window_sizes_ragged_fp8(q_len):
+    # fp8 pools (per-page scales), ragged lengths with partial last pages and a
+    # sequence as short as the window: one to four row tiles, each with its own
+    # ring depth and wavefronts per SIMD, and the whole-row V^T loads
+    w, pool = workload(5, batch=4, seq_len=5000, n_decode=1, n_verify=1)
+    lens = np.array([4000, 3999, 37, q_len], dtype=np.int32)
+    assert np.all((w.full_block_table >= 0).sum(1) * 16 >= lens)
+    g = torch.Generator(device="cuda").manual_seed(100 + q_len)
+    q = (torch.randn((4, q_len, 32, 128), generator=g, device="cuda") / 11.3).to(torch.bfloat16)
+    o, lse = K.verify(kv_of(w), q, dev_i32(lens), dev_i32(w.full_block_table), 4000, 1.0)
+    torch.cuda.synchronize()
+    eo, el = O.verify(pool, q.float().cpu().numpy(), lens, w.full_block_table, 1.0)
+    assert_close("O", o.cpu().numpy(), eo, O_TOL)
+    assert_close("LSE", lse.cpu().numpy(), el, LSE_TOL)
+
+
 def test_window_longer_than_sequence_gives_empty_rows():
     w, pool = workload(2, batch=2, seq_len=100, n_decode=1, n_verify=1)
     w.seq_lens[:] = [3, 100]
