@@ -252,6 +252,15 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     L = a.seq_lens[wi.b];
     nb = max(0, min(a.num_blocks[wi.b], a.max_blocks));
   }
+  // The work item is the same in every lane; saying so keeps it in scalar
+  // registers (the balanced map divides in double precision, whose results
+  // live in vector registers, and a block-table or descriptor address built
+  // from one made the compiler loop over the lanes around every page load).
+  wi.split = __builtin_amdgcn_readfirstlane(wi.split);
+  wi.g = __builtin_amdgcn_readfirstlane(wi.g);
+  wi.b = __builtin_amdgcn_readfirstlane(wi.b);
+  wi.n_split = __builtin_amdgcn_readfirstlane(wi.n_split);
+  wi.slot0 = __builtin_amdgcn_readfirstlane(wi.slot0);
   const int split = wi.split, g = wi.g, b = wi.b, n_split = wi.n_split;
   const int nw = n_split * kWaves;
   const int u = split * kWaves + wave;

@@ -228,6 +228,15 @@ void verify_mfma_kernel(AttnArgs a) {
     wi.slot0 = (blockIdx.z * a.Hkv + blockIdx.y) * a.n_split;
     L = a.seq_lens[wi.b];
   }
+  // The work item is the same in every lane; saying so keeps it in scalar
+  // registers (the balanced map divides in double precision, whose results
+  // live in vector registers, and a block-table or descriptor address built
+  // from one made the compiler loop over the lanes around every page load).
+  wi.split = __builtin_amdgcn_readfirstlane(wi.split);
+  wi.g = __builtin_amdgcn_readfirstlane(wi.g);
+  wi.b = __builtin_amdgcn_readfirstlane(wi.b);
+  wi.n_split = __builtin_amdgcn_readfirstlane(wi.n_split);
+  wi.slot0 = __builtin_amdgcn_readfirstlane(wi.slot0);
   const int split = wi.split, g = wi.g, b = wi.b, n_split = wi.n_split;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
