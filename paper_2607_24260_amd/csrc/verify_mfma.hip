@@ -280,8 +280,9 @@ void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  // RING pair buffers (three, two for fp8; bf16 9..12-token windows two; fp8
-  // 9..12-token windows and 13..16-token windows one),
+  // RING pair buffers (three, two for fp8; 9..12-token windows: bf16 two, fp8
+  // one at two wavefronts per SIMD; 13..16-token windows: bf16 one (two
+  // spill: 478 vs 334 us at 4 x 128K), fp8 two (321 vs 353 us)),
   // unrolled: while one pair is processed the loads of the next ones are in
   // flight. Past the end of this wavefront's pairs the loads go through an
   // empty descriptor (no traffic), so the steady state is straight-line code.
@@ -419,7 +420,7 @@ void verify_mfma_kernel(AttnArgs a) {
     // every round. The block-table entries of the pair a round ahead are read
     // through the vector memory pipe (lanes 0 and 1: pages k and k + 1) right
     // after a slot's pair loads, and used when the slot is refilled next.
-    constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 && KV == kBF16 ? 2 : 1);
+    constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 ? (KV == kBF16 ? 2 : 1) : (KV == kFP8 ? 2 : 1));
     const auto rt = table_rsrc(fbt, np_seq);
     const int voff = (lane & 1) * 4;
     auto second = [&](int k, int v) { return k + 1 < np_seq ? v : -1; };
