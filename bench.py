@@ -421,6 +421,9 @@ def main():
                     help="skip the stream-read ceiling, the context sweep and the TP-share run")
     ap.add_argument("--profile", action="store_true",
                     help="only the timed steps (for rocprofv3 runs)")
+    ap.add_argument("--ragged-only", action="store_true",
+                    help="only the ragged fp8 stream (for rocprofv3 runs of that workload); "
+                         "prints its JSON object")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a 1 GiB device-to-device copy (known bytes for scaling "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -436,6 +439,9 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.ragged_only:
+        print(json.dumps(ragged_stream(torch, K, dev)), flush=True)
+        return
     cfg = args.config
     if cfg == 5:
         print("the ragged fp8 workload is driven by its own accept/fallback schedule; "
