@@ -43,9 +43,9 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kD = 128;
 constexpr int kWaves = 4;
-// pages in flight per wavefront (register ring depth). Two beat three and
-// four on MI355X for both dtypes (128K workload: 24.6 vs 24.9 / 26.9 us per
-// call; ragged fp8 full context: 959 vs 981 / 969 us): a deeper ring does not
+// pages in flight per wavefront (register ring depth). Two beat one and
+// three on MI355X for both dtypes (128K workload: 23.8 vs 26.4 / 24.1 us per
+// call; ragged fp8 full context: 773 vs 799 / 776 us): a deeper ring does not
 // raise the read rate and costs registers and loop overhead.
 #ifndef KAP_DECODE_RING_BF16
 #define KAP_DECODE_RING_BF16 2
