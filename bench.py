@@ -494,34 +494,44 @@ def main():
                          dtype=torch.uint8, device=dev)
     ws_ver = torch.zeros(max(K.verify_workspace_bytes(kvs[0], B, q_len, int(w.seq_lens.max())),
                              256), dtype=torch.uint8, device=dev)
-    dec_calls, ver_calls = [], []
-    for r in range(R):
-        o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
-        l = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-        dec_calls.append([K.bind_selected_decode(kvs[r], w.q_decode[s], seq_lens,
-                                                 plan_out["view_block_table"],
-                                                 plan_out["view_logical_block"],
-                                                 plan_out["view_num_blocks"], cap, w.sm_scale,
-                                                 o, l, ws_dec)
-                          for s in range(w.q_decode.shape[0])])
-        ov = torch.empty((B, q_len, Hq, D), dtype=torch.float32, device=dev)
-        lv = torch.empty((B, q_len, Hq), dtype=torch.float32, device=dev)
-        ver_calls.append([K.bind_verify(kvs[r], w.q_verify[j], seq_lens, fbt,
-                                        int(w.seq_lens.max()), w.sm_scale, ov, lv, ws_ver)
-                          for j in range(len(w.q_verify))])
+    outs = [(torch.empty((B, Hq, D), dtype=torch.float32, device=dev),
+             torch.empty((B, Hq), dtype=torch.float32, device=dev),
+             torch.empty((B, q_len, Hq, D), dtype=torch.float32, device=dev),
+             torch.empty((B, q_len, Hq), dtype=torch.float32, device=dev)) for _ in range(R)]
+
+    def bind_calls(stream):
+        dcs, vcs = [], []
+        for r in range(R):
+            o, l, ov, lv = outs[r]
+            dcs.append([K.bind_selected_decode(kvs[r], w.q_decode[s], seq_lens,
+                                               plan_out["view_block_table"],
+                                               plan_out["view_logical_block"],
+                                               plan_out["view_num_blocks"], cap, w.sm_scale,
+                                               o, l, ws_dec, stream=stream)
+                        for s in range(w.q_decode.shape[0])])
+            vcs.append([K.bind_verify(kvs[r], w.q_verify[j], seq_lens, fbt,
+                                      int(w.seq_lens.max()), w.sm_scale, ov, lv, ws_ver,
+                                      stream=stream)
+                        for j in range(len(w.q_verify))])
+        return dcs, vcs
+
+    dec_calls, ver_calls = bind_calls(None)
 
     sched = w.schedule
     n_dec = sum(1 for k, _ in sched if k == "decode")
     n_ver = len(sched) - n_dec
 
-    def step(_):
-        plan_call()
+    def step_with(pc, dcs, vcs):
+        pc()
         for c, (kind, i) in enumerate(sched):
             r = c % R
             if kind == "decode":
-                dec_calls[r][i]()
+                dcs[r][i]()
             else:
-                ver_calls[r][i]()
+                vcs[r][i]()
+
+    def step(_):
+        step_with(plan_call, dec_calls, ver_calls)
 
     dec_b = algorithmic_bytes(w, view_tokens, view_blocks, "decode")
     ver_b = algorithmic_bytes(w, view_tokens, view_blocks, "verify", q_len)
@@ -550,6 +560,32 @@ def main():
     log(f"step: {ms_step:.3f} ms, {step_b / 1e9:.3f} GB algorithmic -> {value:.1f} GB/s")
     if args.profile:
         return
+
+    # the same step captured as one HIP graph: the calls bound to a side
+    # stream (binding runs each once there), captured, and replayed on it
+    gs = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(gs):
+        g_plan = K.bind_compile_plan(*plan_in, num_pages=w.num_pages, view_capacity=cap,
+                                     out=plan_out, workspace=ws_plan, stream=gs)
+        g_dec, g_ver = bind_calls(gs)
+    gs.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=gs):
+        step_with(g_plan, g_dec, g_ver)
+    with torch.cuda.stream(gs):
+        for _ in range(max(args.warmup, 1)):
+            graph.replay()
+        gs.synchronize()
+        gs_ev, ge_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gs_ev.record(gs)
+        for _ in range(args.steps):
+            graph.replay()
+        ge_ev.record(gs)
+    torch.cuda.synchronize()
+    ms_step_graph = gs_ev.elapsed_time(ge_ev) / args.steps
+    log(f"step as one HIP graph: {ms_step_graph:.3f} ms ({len(sched) + 1} launches per step)")
+    del graph
 
     # per-call rates, rotating replicas (HBM) and on one buffer (cache-hot, context)
     nq = w.q_decode.shape[0]
@@ -704,6 +740,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_graph": round(ms_step_graph, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
