@@ -6,7 +6,7 @@
 // R = 4 * q_len query rows that share every key: a real dense contraction.
 // A workgroup of four wavefronts owns (key split, KV head, sequence); each
 // wavefront walks its share of the split two pages (32 keys) at a time, with
-// the next two page pairs' loads in flight (branch-free, so only the oldest
+// the following page pairs' loads in flight (branch-free, so only the oldest
 // buffer is waited for), using v_mfma_f32_16x16x32_bf16:
 //   S^T[key][row] = K[key][:] . Q[row][:]       A = K tile (16 keys x 32 dims,
 //                                               one 16-byte load per lane; K
@@ -184,9 +184,6 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, in
 }
 
 constexpr int kVerifyWaves = 4;
-// fp8 pairs in flight for windows of up to 8 tokens: two (fewer registers,
-// fewer spills; fp8 pairs are half the bytes of bf16 pairs)
-constexpr int kRingFP8Small = 2;
 
 // Wavefronts per SIMD the compiler must leave room for. fp8 windows of 5-12
 // tokens (two or three row tiles) are issue-bound at one wavefront per SIMD:
@@ -280,9 +277,11 @@ void verify_mfma_kernel(AttnArgs a) {
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
 
-  // RING pair buffers (three, two for fp8; 9..12-token windows: bf16 two, fp8
-  // one at two wavefronts per SIMD; 13..16-token windows: bf16 one (two
-  // spill: 478 vs 334 us at 4 x 128K), fp8 two (321 vs 353 us)),
+  // RING pair buffers (windows of up to 8 tokens: two -- three were 0.2-0.5%
+  // slower for bf16 on MI355X, e.g. 333.0 vs 331.9 us at 128K; 9..12-token
+  // windows: bf16 two, fp8 one at two wavefronts per SIMD; 13..16-token
+  // windows: bf16 one (two spill: 478 vs 334 us at 4 x 128K), fp8 two (321 vs
+  // 353 us)),
   // unrolled: while one pair is processed the loads of the next ones are in
   // flight. Past the end of this wavefront's pairs the loads go through an
   // empty descriptor (no traffic), so the steady state is straight-line code.
@@ -420,7 +419,7 @@ void verify_mfma_kernel(AttnArgs a) {
     // every round. The block-table entries of the pair a round ahead are read
     // through the vector memory pipe (lanes 0 and 1: pages k and k + 1) right
     // after a slot's pair loads, and used when the slot is refilled next.
-    constexpr int RING = NT <= 2 ? (KV == kFP8 ? kRingFP8Small : 3) : (NT == 3 ? (KV == kBF16 ? 2 : 1) : (KV == kFP8 ? 2 : 1));
+    constexpr int RING = NT <= 2 ? 2 : (NT == 3 ? (KV == kBF16 ? 2 : 1) : (KV == kFP8 ? 2 : 1));
     const auto rt = table_rsrc(fbt, np_seq);
     const int voff = (lane & 1) * 4;
     auto second = [&](int k, int v) { return k + 1 < np_seq ? v : -1; };
