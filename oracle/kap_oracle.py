@@ -22,6 +22,10 @@ Systems" (arXiv 2607.24260). What is computed, and where it is defined:
   workspace of fixed capacity.
 * ``accept_top_k`` -- Sec. 3.2 target-guided tolerant verification (the
   Top-3 rule): accepted prefix length and the verifier's carry token.
+* ``access_modes`` / ``active_view`` -- Sec. 3.2, "Runtime stability and
+  fallback": per cycle, whether a sequence's proposal steps read its plan's
+  view or the full context (h from Eq. (5) against s from Eq. (4), the
+  margin condition h > s of Eq. (12)), and the view rows that mode reads.
 * ``lse_merge`` -- the exact softmax identity used to combine attention over
   disjoint key sets (a standard identity, not stated in the paper).
 * ``e4m3fn_to_f64`` / ``bf16_to_f64`` -- decoding of stored KV bits (OCP 8-bit
@@ -39,12 +43,17 @@ h // (Hq / Hkv).
 
 Parity status: every function here is pinned by a CPU test against something
 other than itself (hand-worked vectors, closed forms, brute force, torch
-library routines, invariants); see tests/test_oracle_*.py.
+library routines, invariants); see tests/test_oracle_*.py. The access-mode
+policy's window length, its first-cycle grace and its stickiness are this
+oracle's reading (the paper names the fallback conditions but gives no
+thresholds): its pins fix that stated rule, and parity with the paper's own
+thresholds is unpinned.
 """
 from __future__ import annotations
 
 import math
 from dataclasses import dataclass
+from fractions import Fraction
 from typing import Optional, Sequence
 
 import numpy as np
@@ -402,10 +411,16 @@ def selected_decode(pool: KVPool, q: np.ndarray, seq_lens, view_block_table,
 
 
 def full_tokens(pool: KVPool, g: int, seq_len: int, fbt_row):
-    """K and V of all tokens 0 .. seq_len-1 of one sequence, in logical order."""
+    """K, V and logical positions of the tokens 0 .. seq_len-1 of one
+    sequence, in logical order. A page whose id lies outside the pool
+    contributes no keys (as for views), so its positions are absent."""
     npages = -(-int(seq_len) // PAGE)
-    pages = np.asarray(fbt_row)[:npages]
-    return _view_tokens(pool, g, int(seq_len), pages, np.arange(npages), skip_invalid=False)
+    pages = np.asarray(fbt_row, dtype=np.int64)[:npages]
+    k, v = _view_tokens(pool, g, int(seq_len), pages, np.arange(npages))
+    ok = (pages >= 0) & (pages < pool.k_pages.shape[0])
+    grid = PAGE * np.arange(npages)[:, None] + np.arange(PAGE)[None, :]   # [page][token]
+    pos = grid[ok[:, None] & (grid < int(seq_len))]                        # row-major: ascending
+    return k, v, pos
 
 
 def verify(pool: KVPool, q: np.ndarray, seq_lens, full_block_table,
@@ -415,10 +430,10 @@ def verify(pool: KVPool, q: np.ndarray, seq_lens, full_block_table,
 
     q: [B][q_len][Hq][D]: the carry token and the k proposed tokens. Their K/V
     are the last q_len tokens of the cache, so seq_lens[b] counts them. Window
-    row i sees logical positions 0 .. seq_lens[b] - q_len + i (causal among the
-    window). Returns o [B][q_len][Hq][D] and lse [B][q_len][Hq] in float64.
-    ``batches`` / ``kv_heads`` restrict the work to a subset (other entries
-    are left as o = 0, lse = -inf).
+    row i sees the keys at logical positions 0 .. seq_lens[b] - q_len + i
+    (causal among the window). Returns o [B][q_len][Hq][D] and lse
+    [B][q_len][Hq] in float64. ``batches`` / ``kv_heads`` restrict the work to
+    a subset (other entries are left as o = 0, lse = -inf).
     """
     q = np.asarray(q, dtype=np.float64)
     B, QL, Hq, D = q.shape
@@ -428,9 +443,10 @@ def verify(pool: KVPool, q: np.ndarray, seq_lens, full_block_table,
     lse = np.full((B, QL, Hq), -np.inf)
     for b in (range(B) if batches is None else batches):
         L = int(seq_lens[b])
-        nvis = [L - QL + i + 1 for i in range(QL)]
         for g in (range(Hkv) if kv_heads is None else kv_heads):
-            k, v = full_tokens(pool, g, L, full_block_table[b])
+            k, v, pos = full_tokens(pool, g, L, full_block_table[b])
+            # keys are in ascending position: row i sees a prefix of them
+            nvis = [int(np.sum(pos <= L - QL + i)) for i in range(QL)]
             for h in range(g * G, (g + 1) * G):
                 ob, lb = attend(q[b, :, h], k, v, nvis, sm_scale)
                 o[b, :, h] = ob
@@ -544,6 +560,82 @@ def compact_view(pool: KVPool, view_block_table, view_num_blocks, capacity: int)
                 sc[dst] = pool.scales[p]
             table[b, j] = dst
     return KVPool(k, v, pool.dtype, sc), table
+
+
+# --------------------------------------------------------------------------
+# Access mode per cycle: the selected view or full-context fallback
+# --------------------------------------------------------------------------
+
+SELECTED = 0   # proposal steps read the plan's selected-KV view
+FULL = 1       # proposal steps read the whole context
+
+
+def access_modes(plan_status, view_tokens, seq_lens, accepted, gammas, window: int):
+    """Access mode of every sequence at the start and after each cycle.
+
+    Sec. 3.2 ("Runtime stability and fallback") has the executor read the
+    full context instead of the plan when the plan cannot be executed (it
+    exceeds the compact workspace, or is otherwise unusable) or when the
+    observed acceptance is low for the KV the plan retains. The quantities
+    are s, the retained ratio of Eq. (4) -- here view_tokens[b] / seq_lens[b],
+    the proposal path's visible tokens over the full context's -- and h, the
+    acceptance rate of Eq. (5), accepted over speculated proposed tokens;
+    Eq. (12) gives h > s as the condition for a positive KV-access margin.
+
+    Reading used (the paper names the conditions, not thresholds):
+      * a sequence starts on its plan (SELECTED) iff plan_status[b] is OK
+        (0), else on the full context (FULL);
+      * cycle c speculates gammas[c] tokens per sequence, of which
+        min(max(accepted[c][b], 0), gammas[c]) are accepted;
+      * once a sequence has completed at least two cycles, h is taken over
+        its last ``window`` cycles (sum accepted / sum speculated); if that
+        sum speculated is positive and h <= s, the sequence switches to FULL;
+      * FULL is kept for the rest of the run.
+    h and s are compared as exact rationals.
+
+    accepted: [C][B] integers, gammas: [C]. Returns an int64 array
+    [C + 1][B]: row 0 holds the modes before the first cycle, row c + 1 the
+    modes after cycle c.
+    """
+    B = len(seq_lens)
+    C = len(gammas)
+    modes = np.zeros((C + 1, B), dtype=np.int64)
+    for b in range(B):
+        mode = SELECTED if int(plan_status[b]) == PLAN_OK else FULL
+        modes[0, b] = mode
+        history = []                     # (accepted, speculated) per cycle
+        s = Fraction(int(view_tokens[b]), int(seq_lens[b])) if int(seq_lens[b]) > 0 else None
+        for c in range(C):
+            g = int(gammas[c])
+            a = min(max(int(accepted[c][b]), 0), g)
+            history.append((a, g))
+            if mode == SELECTED and len(history) >= 2 and s is not None:
+                recent = history[-window:]
+                acc = sum(x for x, _ in recent)
+                spec = sum(y for _, y in recent)
+                if spec > 0 and Fraction(acc, spec) <= s:
+                    mode = FULL
+            modes[c + 1, b] = mode
+    return modes
+
+
+def active_view(mode: int, plan: Plan, full_block_table_row, seq_len: int):
+    """The view rows a proposal step of one sequence reads in a given mode.
+
+    SELECTED: the plan's view (its physical pages, logical pages and, for a
+    token-granular plan, its token masks). FULL: every page of the context
+    that the full block table holds, in logical order, each with all 16
+    tokens marked visible. Returns (block_table, logical_blocks, num_blocks,
+    token_masks) as lists; token_masks is None for a page-granular plan.
+    """
+    masked = plan.token_masks is not None
+    if mode == SELECTED:
+        n = plan.num_blocks
+        masks = list(plan.token_masks[:n]) if masked else None
+        return list(plan.block_table[:n]), list(plan.logical_blocks[:n]), n, masks
+    row = list(full_block_table_row)
+    n = min(-(-int(seq_len) // PAGE), len(row)) if seq_len > 0 else 0
+    return row[:n], list(range(n)), n, ([0xFFFF] * n if masked else None)
 
 
 # --------------------------------------------------------------------------
