@@ -419,3 +419,64 @@ def test_planted_causal_off_by_one_is_caught(monkeypatch):
         m.setattr(O, "attend", lambda q_, k, v, nv, s: orig(q_, k, v, [n - 1 for n in nv], s))
         o, _ = O.verify(pool, q, seq_lens, fbt, 1.0)
     assert np.abs(o - eo).max() > 1e-3
+
+
+# --------------------------------------------------------------------------
+# page ids outside the pool contribute no keys
+# --------------------------------------------------------------------------
+
+def _masked_brute_verify(pool, q, seq_lens, fbt, sm_scale):
+    """brute_verify with the positions of out-of-pool pages masked out (their
+    ids replaced by page 0 only to gather something, then hidden)."""
+    nP = pool.k_pages.shape[0]
+    B, QL, Hq, D = q.shape
+    G = Hq // pool.k_pages.shape[1]
+    o = np.zeros((B, QL, Hq, D))
+    lse = np.zeros((B, QL, Hq))
+    for b in range(B):
+        L = int(seq_lens[b])
+        row = np.asarray(fbt[b], dtype=np.int64)
+        bad = (row < 0) | (row >= nP)
+        K, V = logical_kv(pool, np.where(bad, 0, row), L)
+        K, V = K.repeat_interleave(G, 0), V.repeat_interleave(G, 0)
+        pos = torch.arange(L)
+        shown = ~torch.as_tensor(bad)[pos // P]
+        mask = (pos[None, :] <= (L - QL + torch.arange(QL))[:, None]) & shown[None, :]
+        qq = torch.as_tensor(np.asarray(q[b], dtype=np.float64)).transpose(0, 1)
+        ob, lb = sdpa_rows(qq, K, V, mask, sm_scale)
+        o[b] = ob.transpose(0, 1).nan_to_num(0.0).numpy()
+        lse[b] = lb.transpose(0, 1).numpy()
+    return o, lse
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_verify_out_of_pool_pages_contribute_no_keys(dtype):
+    rng = np.random.default_rng(5)
+    pool = make_pool(12, 2, 16, dtype, seed=9)
+    seq_lens = np.array([70, 33, 20])
+    fbt = rng.integers(0, 12, (3, 5))
+    fbt[0, 1], fbt[0, 4] = 12, -1          # an inner page and the last page
+    fbt[1, 0] = 40                          # the first page
+    fbt[2, 1] = -7                          # the last page: the window's own keys
+    q = rng.standard_normal((3, 4, 8, 16))
+    eo, el = O.verify(pool, q, seq_lens, fbt, 0.3)
+    bo, bl = _masked_brute_verify(pool, q, seq_lens, fbt, 0.3)
+    assert np.abs(eo - bo).max() < 1e-12
+    fin = np.isfinite(bl)
+    assert np.array_equal(fin, np.isfinite(el)) and np.abs(el[fin] - bl[fin]).max() < 1e-12
+    # sequence 2's last page (tokens 16..19) is out of the pool: every row sees
+    # exactly tokens 0..15, as a one-page sequence of 16 tokens whose window
+    # rows all see the whole page
+    assert np.all(fin[2])
+    for i in range(4):
+        one = O.selected_decode(pool, q[2, i][None], [16], [[fbt[2, 0]]], [[0]], [1], 0.3)
+        assert np.abs(eo[2, i] - one[0][0]).max() < 1e-12
+
+
+def test_decode_out_of_pool_pages_contribute_no_keys():
+    pool = make_pool(6, 2, 16, "bf16", seed=2)
+    q = np.random.default_rng(1).standard_normal((1, 8, 16))
+    full = O.selected_decode(pool, q, [40], [[3, 1, 5]], [[0, 1, 2]], [3], 0.5)
+    part = O.selected_decode(pool, q, [40], [[3, 9, 5, -2]], [[0, 1, 2, 1]], [4], 0.5)
+    only = O.selected_decode(pool, q, [40], [[3, 5]], [[0, 2]], [2], 0.5)
+    assert np.abs(part[0] - only[0]).max() < 1e-15 and np.abs(full[0] - only[0]).max() > 1e-3
