@@ -47,14 +47,8 @@ constexpr int kWaves = 4;
 // three on MI355X for both dtypes (128K workload: 23.8 vs 26.4 / 24.1 us per
 // call; ragged fp8 full context: 773 vs 799 / 776 us): a deeper ring does not
 // raise the read rate and costs registers and loop overhead.
-#ifndef KAP_DECODE_RING_BF16
-#define KAP_DECODE_RING_BF16 2
-#endif
-#ifndef KAP_DECODE_RING_FP8
-#define KAP_DECODE_RING_FP8 2
-#endif
-constexpr int kRingBF16 = KAP_DECODE_RING_BF16;
-constexpr int kRingFP8 = KAP_DECODE_RING_FP8;
+constexpr int kRingBF16 = 2;
+constexpr int kRingFP8 = 2;
 
 // D += A B on 16 blocks of 4x4 (K = 4, bf16 operands, fp32 accumulation):
 // block b = lane / 4; A row i of block b comes from lane 4 b + i, B column j

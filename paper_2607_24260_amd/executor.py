@@ -77,8 +77,9 @@ class FallbackPolicy:
 
 
 def accepted_counts(draws: np.ndarray, gamma: int) -> np.ndarray:
-    """m = min(X, gamma) for draws X >= 0 (m in {0, ..., gamma}, Eq. (2))."""
-    return np.minimum(np.asarray(draws, dtype=np.int64), int(gamma))
+    """m = min(max(X, 0), gamma) for accept draws X (m in {0, ..., gamma},
+    Eq. (2)); the device policy clamps the same way."""
+    return np.clip(np.asarray(draws, dtype=np.int64), 0, int(gamma))
 
 
 class ViewBuilder:
@@ -132,10 +133,19 @@ def run_stream(w, kv, plan: dict, *, window: int = 4, keep_outputs: Optional[set
 
     `plan` holds the compiled plan tensors (see kap.compile_plan). The plan's
     view_tokens are read back once to form s_b. Outputs of the calls named in
-    keep_outputs ({('decode', i), ('verify', j)}) are kept (cloned)."""
+    keep_outputs ({('decode', i), ('verify', j)}) are kept (cloned).
+
+    With ``stream``, everything -- the library calls, the view switches and
+    the output copies -- is enqueued on that stream (it becomes torch's
+    current stream for the run), so the host-side tensor work stays ordered
+    with the kernels."""
     import torch
 
     from . import kap as K
+
+    if stream is not None:
+        with torch.cuda.stream(stream):
+            return run_stream(w, kv, plan, window=window, keep_outputs=keep_outputs)
 
     dev = kv.device
     i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32)).to(dev)
@@ -160,13 +170,12 @@ def run_stream(w, kv, plan: dict, *, window: int = 4, keep_outputs: Optional[set
     for kind, idx in w.schedule:
         if kind == "decode":
             K.selected_decode(kv, w.q_decode[idx], seq_lens, views.vbt, views.vlb, views.vnb,
-                              views.max_blocks, w.sm_scale, out=out, lse=lse, workspace=ws_dec,
-                              stream=stream)
+                              views.max_blocks, w.sm_scale, out=out, lse=lse, workspace=ws_dec)
             if ("decode", idx) in keep:
                 dec_res.append((idx, out.clone(), lse.clone(), policy.mode.copy()))
         else:
             q = w.q_verify[idx]
-            ov, lv = K.verify(kv, q, seq_lens, fbt, max_len, w.sm_scale, stream=stream)
+            ov, lv = K.verify(kv, q, seq_lens, fbt, max_len, w.sm_scale)
             if ("verify", idx) in keep:
                 ver_res.append((idx, ov, lv))
             g = gammas[idx]
@@ -203,54 +212,61 @@ class DeviceStream:
         self.torch = torch
         dev = kv.device
         self.stream = stream if stream is not None else torch.cuda.Stream(device=dev)
-        i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32)).to(dev)
-        B = w.batch
-        self.w = w
-        self.plan_call = plan_call
-        self.seq_lens = i32(w.seq_lens)
-        self.fbt = i32(w.full_block_table)
-        cap = plan["view_block_table"].shape[1]
-        stride = max(int(self.fbt.shape[1]), int(cap))
-        self.vbt = torch.zeros((B, stride), dtype=torch.int32, device=dev)
-        self.vlb = torch.zeros((B, stride), dtype=torch.int32, device=dev)
-        self.vnb = torch.zeros(B, dtype=torch.int32, device=dev)
-        tok = "view_token_mask" in plan
-        self.vmask = torch.zeros((B, stride), dtype=torch.int32, device=dev) if tok else None
-        masks = dict(sel_token_mask=plan["view_token_mask"], view_token_mask=self.vmask) \
-            if tok else {}
-        self.history = torch.zeros((B, window, 2), dtype=torch.int32, device=dev)
-        self.cycles = torch.zeros(B, dtype=torch.int32, device=dev)
-        self.mode = torch.zeros(B, dtype=torch.int32, device=dev)
-        self.draws = i32(w.accept_draws)                        # [cycles][B]
-        self.gammas = [q.shape[1] - 1 for q in w.q_verify]
-        common = (plan["view_tokens"], self.seq_lens, plan["plan_status"], self.history,
-                  self.cycles, self.mode, plan["view_block_table"], plan["view_logical_block"],
-                  plan["view_num_blocks"], self.fbt, self.vbt, self.vlb, self.vnb)
-        s = self.stream
-        self.reset = K.bind_fallback_update(True, window, 0, None, *common, stream=s, **masks)
-        self.update = [K.bind_fallback_update(False, window, g, self.draws[c], *common, stream=s,
-                                              **masks)
-                       for c, g in enumerate(self.gammas)]
-        Hq, D = w.num_q_heads, w.head_dim
-        self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
-        self.lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
-        ws = torch.zeros(max(256, K.selected_decode_workspace_bytes(kv, B, stride)),
-                         dtype=torch.uint8, device=dev)
-        self.decode = [K.bind_selected_decode(kv, w.q_decode[i], self.seq_lens, self.vbt,
-                                              self.vlb, self.vnb, stride, w.sm_scale, self.out,
-                                              self.lse, ws, view_token_mask=self.vmask, stream=s)
-                       for i in range(w.q_decode.shape[0])]
-        max_len = int(np.max(w.seq_lens))
-        self.ver_out, self.verify = [], []
-        for q in w.q_verify:
-            ql = q.shape[1]
-            ov = torch.empty((B, ql, Hq, D), dtype=torch.float32, device=dev)
-            lv = torch.empty((B, ql, Hq), dtype=torch.float32, device=dev)
-            wv = torch.zeros(max(256, K.verify_workspace_bytes(kv, B, ql, max_len)),
+        # the inputs were made on the current stream; everything allocated
+        # here is made (and zero-filled) on self.stream, where the bound
+        # calls run -- binding validates each call by launching it once
+        self.stream.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(self.stream):
+            i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32)).to(dev)
+            B = w.batch
+            self.w = w
+            self.plan_call = plan_call
+            self.seq_lens = i32(w.seq_lens)
+            self.fbt = i32(w.full_block_table)
+            cap = plan["view_block_table"].shape[1]
+            stride = max(int(self.fbt.shape[1]), int(cap))
+            self.vbt = torch.zeros((B, stride), dtype=torch.int32, device=dev)
+            self.vlb = torch.zeros((B, stride), dtype=torch.int32, device=dev)
+            self.vnb = torch.zeros(B, dtype=torch.int32, device=dev)
+            tok = "view_token_mask" in plan
+            self.vmask = torch.zeros((B, stride), dtype=torch.int32, device=dev) if tok else None
+            masks = dict(sel_token_mask=plan["view_token_mask"], view_token_mask=self.vmask) \
+                if tok else {}
+            self.history = torch.zeros((B, window, 2), dtype=torch.int32, device=dev)
+            self.cycles = torch.zeros(B, dtype=torch.int32, device=dev)
+            self.mode = torch.zeros(B, dtype=torch.int32, device=dev)
+            self.draws = i32(w.accept_draws)                        # [cycles][B]
+            self.gammas = [q.shape[1] - 1 for q in w.q_verify]
+            common = (plan["view_tokens"], self.seq_lens, plan["plan_status"], self.history,
+                      self.cycles, self.mode, plan["view_block_table"],
+                      plan["view_logical_block"], plan["view_num_blocks"], self.fbt, self.vbt,
+                      self.vlb, self.vnb)
+            s = self.stream
+            self.reset = K.bind_fallback_update(True, window, 0, None, *common, stream=s, **masks)
+            self.update = [K.bind_fallback_update(False, window, g, self.draws[c], *common,
+                                                  stream=s, **masks)
+                           for c, g in enumerate(self.gammas)]
+            Hq, D = w.num_q_heads, w.head_dim
+            self.out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+            self.lse = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+            ws = torch.zeros(max(256, K.selected_decode_workspace_bytes(kv, B, stride)),
                              dtype=torch.uint8, device=dev)
-            self.ver_out.append((ov, lv))
-            self.verify.append(K.bind_verify(kv, q, self.seq_lens, self.fbt, max_len, w.sm_scale,
-                                             ov, lv, wv, stream=s))
+            self.decode = [K.bind_selected_decode(kv, w.q_decode[i], self.seq_lens, self.vbt,
+                                                  self.vlb, self.vnb, stride, w.sm_scale,
+                                                  self.out, self.lse, ws,
+                                                  view_token_mask=self.vmask, stream=s)
+                           for i in range(w.q_decode.shape[0])]
+            max_len = int(np.max(w.seq_lens))
+            self.ver_out, self.verify = [], []
+            for q in w.q_verify:
+                ql = q.shape[1]
+                ov = torch.empty((B, ql, Hq, D), dtype=torch.float32, device=dev)
+                lv = torch.empty((B, ql, Hq), dtype=torch.float32, device=dev)
+                wv = torch.zeros(max(256, K.verify_workspace_bytes(kv, B, ql, max_len)),
+                                 dtype=torch.uint8, device=dev)
+                self.ver_out.append((ov, lv))
+                self.verify.append(K.bind_verify(kv, q, self.seq_lens, self.fbt, max_len,
+                                                 w.sm_scale, ov, lv, wv, stream=s))
 
     def run(self):
         """Enqueue one whole stream on self.stream (no host synchronisation)."""

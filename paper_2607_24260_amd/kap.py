@@ -2,9 +2,12 @@
 
 Every function here checks tensor placement, dtype and shape, allocates
 outputs / workspace with torch when the caller does not pass them, and calls
-the matching ``kap_*`` entry point of ``libkap.so`` on torch's current HIP
-stream. All computation happens in the library's HIP kernels; there is no CPU
-path. A missing library or a CPU tensor raises.
+the matching ``kap_*`` entry point of ``libkap.so`` on the given stream
+(torch's current HIP stream by default). Tensors allocated here are allocated,
+and zero-filled where needed, on that same stream, so they are ordered with
+the launch and the caching allocator reuses them only after it. All
+computation happens in the library's HIP kernels; there is no CPU path. A
+missing library or a CPU tensor raises.
 """
 from __future__ import annotations
 
@@ -179,9 +182,11 @@ def _stream(stream):
 
 
 def _workspace(nbytes: int, device, workspace: Optional[torch.Tensor]):
+    """Caller's workspace, or a zero-filled temporary (the arrival counters
+    must start at 0). Call under ``torch.cuda.stream(launch stream)``."""
     if nbytes == 0:
         return workspace, 0
-    if workspace is None:       # zero-filled: the arrival counters must start at 0
+    if workspace is None:
         workspace = torch.zeros(nbytes, dtype=torch.uint8, device=device)
     _dev(workspace, "workspace")
     have = workspace.numel() * workspace.element_size()
@@ -278,7 +283,8 @@ def compact_view(src: KVCache, view_block_table, view_num_blocks, view_capacity:
     if view_block_table.shape[0] != B:
         raise ValueError("view_block_table and view_num_blocks disagree on the batch")
     if out is None:
-        out = torch.empty((B, view_capacity), dtype=torch.int32, device=src.device)
+        with torch.cuda.stream(stream):
+            out = torch.empty((B, view_capacity), dtype=torch.int32, device=src.device)
     _dev(out, "out", torch.int32, 2)
     if tuple(out.shape) != (B, view_capacity):
         raise ValueError(f"out must be {(B, view_capacity)}")
@@ -370,13 +376,15 @@ def accept_top3(logits, draft_tokens, top_k: int = 3, accepted=None, carry=None,
     if tuple(draft_tokens.shape) != (B, Wn - 1):
         raise ValueError(f"draft_tokens must be {(B, Wn - 1)}")
     dev = logits.device
-    if accepted is None:
-        accepted = torch.empty(B, dtype=torch.int32, device=dev)
-    if carry is None:
-        carry = torch.empty(B, dtype=torch.int32, device=dev)
+    with torch.cuda.stream(stream):
+        if accepted is None:
+            accepted = torch.empty(B, dtype=torch.int32, device=dev)
+        if carry is None:
+            carry = torch.empty(B, dtype=torch.int32, device=dev)
+        workspace, have = _workspace(int(lib.kap_accept_top3_workspace_bytes(B, Wn)), dev,
+                                     workspace)
     _dev(accepted, "accepted", torch.int32, 1)
     _dev(carry, "carry", torch.int32, 1)
-    workspace, have = _workspace(int(lib.kap_accept_top3_workspace_bytes(B, Wn)), dev, workspace)
     dt = KAP_DT_F32 if logits.dtype == torch.float32 else KAP_DT_BF16
     _check(lib.kap_accept_top3(B, Wn, V, _ptr(logits), dt, _ptr(draft_tokens), int(top_k),
                                _ptr(accepted), _ptr(carry), _ptr(workspace), have,
@@ -419,19 +427,22 @@ def _plan_call(seq_lens, full_block_table, span_offsets, span_start, span_len, s
         if t.shape[0] != B:
             raise ValueError(f"{name} must have batch entries")
     dev = seq_lens.device
-    if out is None:
-        cap = max(int(view_capacity), 0)
-        out = {
-            "view_block_table": torch.empty((B, cap), dtype=i32, device=dev),
-            "view_logical_block": torch.empty((B, cap), dtype=i32, device=dev),
-            "view_num_blocks": torch.empty(B, dtype=i32, device=dev),
-            "view_tokens": torch.empty(B, dtype=i32, device=dev),
-            "spans_taken": torch.empty(B, dtype=i32, device=dev),
-            "plan_status": torch.empty(B, dtype=i32, device=dev),
-            "span_selected": torch.empty(S, dtype=i32, device=dev),
-        }
-        if token_granular:
-            out["view_token_mask"] = torch.empty((B, cap), dtype=i32, device=dev)
+    with torch.cuda.stream(stream):
+        if out is None:
+            cap = max(int(view_capacity), 0)
+            out = {
+                "view_block_table": torch.empty((B, cap), dtype=i32, device=dev),
+                "view_logical_block": torch.empty((B, cap), dtype=i32, device=dev),
+                "view_num_blocks": torch.empty(B, dtype=i32, device=dev),
+                "view_tokens": torch.empty(B, dtype=i32, device=dev),
+                "spans_taken": torch.empty(B, dtype=i32, device=dev),
+                "plan_status": torch.empty(B, dtype=i32, device=dev),
+                "span_selected": torch.empty(S, dtype=i32, device=dev),
+            }
+            if token_granular:
+                out["view_token_mask"] = torch.empty((B, cap), dtype=i32, device=dev)
+        need = compile_plan_workspace_bytes(B, S, full_block_table.shape[1])
+        workspace, have = _workspace(need, dev, workspace)
     tables = ("view_block_table", "view_logical_block") + (
         ("view_token_mask",) if token_granular else ())
     for name in tables:
@@ -440,8 +451,6 @@ def _plan_call(seq_lens, full_block_table, span_offsets, span_start, span_len, s
         _dev(out[name], name, i32, 2)
         if out[name].shape != (B, view_capacity):
             raise ValueError(f"{name} must be [batch][view_capacity]")
-    need = compile_plan_workspace_bytes(B, S, full_block_table.shape[1])
-    workspace, have = _workspace(need, dev, workspace)
     head = (B, _ptr(seq_lens), _ptr(full_block_table), full_block_table.shape[1],
             _ptr(span_offsets), S, _ptr(span_start), _ptr(span_len), _ptr(span_prior),
             _ptr(prefix_tokens), _ptr(suffix_tokens), _ptr(budget_tokens), int(policy),
@@ -524,9 +533,10 @@ def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
             raise ValueError("view_token_mask must be shaped like the view tables")
     if seq_lens.shape[0] != B or view_num_blocks.shape[0] != B:
         raise ValueError("seq_lens / view_num_blocks must have batch entries")
-    out, lse = _outputs((B, kv.num_q_heads, kv.head_dim), q.device, out, lse)
     need = selected_decode_workspace_bytes(kv, B, max_view_blocks, num_splits)
-    workspace, have = _workspace(need, q.device, workspace)
+    with torch.cuda.stream(stream):
+        out, lse = _outputs((B, kv.num_q_heads, kv.head_dim), q.device, out, lse)
+        workspace, have = _workspace(need, q.device, workspace)
     head = (ctypes.byref(kv.struct), B, _ptr(q), _ptr(seq_lens), _ptr(view_block_table),
             _ptr(view_logical_block))
     mask = () if view_token_mask is None else (_ptr(view_token_mask),)
@@ -567,9 +577,10 @@ def verify(kv: KVCache, q, seq_lens, full_block_table, max_seq_len: int, sm_scal
     _dev(full_block_table, "full_block_table", torch.int32, 2)
     if seq_lens.shape[0] != B or full_block_table.shape[0] != B:
         raise ValueError("seq_lens / full_block_table must have batch rows")
-    out, lse = _outputs((B, q_len, kv.num_q_heads, kv.head_dim), q.device, out, lse)
     need = verify_workspace_bytes(kv, B, q_len, max_seq_len, num_splits)
-    workspace, have = _workspace(need, q.device, workspace)
+    with torch.cuda.stream(stream):
+        out, lse = _outputs((B, q_len, kv.num_q_heads, kv.head_dim), q.device, out, lse)
+        workspace, have = _workspace(need, q.device, workspace)
     st = lib.kap_verify(
         ctypes.byref(kv.struct), B, q_len, _ptr(q), _ptr(seq_lens), _ptr(full_block_table),
         full_block_table.shape[1], int(max_seq_len), float(sm_scale), int(num_splits),

@@ -57,3 +57,30 @@ def test_mixed_gamma_acceptance_is_token_weighted():
     p.update([0], 8)                 # (2 + 0) / (2 + 8) = 0.2 <= 0.4
     assert p.mode[0] == FULL
     assert abs(p.acceptance(0) - 0.2) < 1e-12
+
+
+def test_negative_draws_clamp_to_zero():
+    assert list(accepted_counts([-3, 2], 4)) == [0, 2]
+
+
+def test_host_policy_matches_the_oracle_on_random_streams():
+    # the executor's host policy against the oracle's access_modes, cycle by
+    # cycle, over random plans (some failed), windows, gammas and accepts
+    from oracle import kap_oracle as O
+
+    rng = np.random.default_rng(11)
+    for trial in range(80):
+        B = int(rng.integers(1, 9))
+        C = int(rng.integers(0, 12))
+        w = int(rng.integers(1, 7))
+        L = rng.integers(1, 5000, B)
+        V = np.minimum(rng.integers(0, 5000, B), L)
+        st = np.where(rng.random(B) < 0.2, O.PLAN_OVER_CAPACITY, O.PLAN_OK)
+        gam = rng.choice([0, 1, 2, 4, 8], C)
+        acc = rng.integers(-1, 10, (C, B))
+        want = O.access_modes(st, V, L, acc, gam, w)
+        p = FallbackPolicy(V / L.astype(np.float64), st == O.PLAN_OK, window=w)
+        assert np.array_equal(p.mode, want[0]), trial
+        for c in range(C):
+            p.update(accepted_counts(acc[c], gam[c]), int(gam[c]))
+            assert np.array_equal(p.mode, want[c + 1]), (trial, c)

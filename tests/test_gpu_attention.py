@@ -153,6 +153,13 @@ def test_config4_verify_sampled():
     verify_check(w, pool, [0, 1], batches=[0, 3], kv_heads=[0, 7])
 
 
+def test_config4_verify_full_width():
+    # one whole 128K verify call: all 4 sequences x 8 KV heads x 4 query
+    # heads x 5 window rows against the oracle
+    w, pool = workload(4, n_verify=2)
+    verify_check(w, pool, [1])
+
+
 def test_config5_fp8_decode():
     # decode steps 0 and last, all 64 ragged sequences on the GPU; the oracle
     # checks every fourth sequence (0, 4, ..., 60)
@@ -337,3 +344,87 @@ def test_peaky_planted_keys(alpha, kv_dtype):
     qv = w.q_decode[0][:, None].repeat(1, 3, 1, 1).contiguous()
     w.q_verify = [qv]
     verify_check(w, pool, [0])
+
+
+# --------------------------------------------------------------------------
+# every geometry the ABI accepts: the generic path (any GQA ratio, head_dim
+# 64 / 128 / 256) for bf16 and fp8 pools, one and several key splits
+# --------------------------------------------------------------------------
+
+def _ragged(cfg, batch, seq_len, lens, **kw):
+    """Workload with its lengths replaced by the (shorter) ragged ones."""
+    w, _ = workload(cfg, batch=batch, seq_len=seq_len, n_decode=1, n_verify=1, **kw)
+    lens = np.asarray(lens, dtype=np.int32)
+    assert np.all((w.full_block_table >= 0).sum(1) * 16 >= lens)
+    w.seq_lens[:] = lens
+    _CACHE.clear()
+    return w, oracle_pool(w)
+
+
+def _window(w, q_len, seed):
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    x = torch.randn((w.batch, q_len, w.num_q_heads, w.head_dim), generator=g, device="cuda")
+    return (x / float(np.sqrt(w.head_dim))).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("D,Hq,Hkv", [(64, 8, 4), (256, 16, 2), (128, 16, 8), (128, 32, 4)])
+@pytest.mark.parametrize("L,num_splits", [(900, 0), (3000, 0), (3000, 7)])
+def test_generic_path_geometries(kv_dtype, D, Hq, Hkv, L, num_splits):
+    # lengths L, L - 1 and 37 (partial last pages); 900 tokens fit one generic
+    # split (<= 64 pages), 3000 take three, num_splits = 7 forces seven
+    cfg = 2 if kv_dtype == "bf16" else 5
+    # (the ragged fp8 recipe draws its lengths from [4096, seq_len])
+    w, pool = _ragged(cfg, 3, max(L, 1000) if cfg == 2 else 5000, [L, L - 1, 37],
+                      num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D)
+    decode_check(w, pool, [0], num_splits=num_splits)
+    q = _window(w, 5, D + Hq + L)
+    o, lse = K.verify(kv_of(w), q, dev_i32(w.seq_lens), dev_i32(w.full_block_table), L, 1.0,
+                      num_splits=num_splits)
+    torch.cuda.synchronize()
+    eo, el = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, w.full_block_table, 1.0)
+    assert_close("generic verify O", o.cpu().numpy(), eo, O_TOL)
+    assert_close("generic verify LSE", lse.cpu().numpy(), el, LSE_TOL)
+
+
+# --------------------------------------------------------------------------
+# page ids outside [0, num_pages) contribute no keys
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kv_dtype,D", [("bf16", 128), ("fp8", 128), ("bf16", 64), ("fp8", 256)])
+def test_out_of_pool_page_ids_contribute_no_keys(kv_dtype, D):
+    # the library is told the pool holds fewer pages than the tensors do, so
+    # the ids past that count name allocated memory that must still not be
+    # read; views and tables also carry negative ids. D = 128 runs the tuned
+    # kernels, D = 64 / 256 the generic path.
+    cfg = 2 if kv_dtype == "bf16" else 5
+    w, _ = workload(cfg, batch=3, seq_len=5000, n_decode=1, n_verify=1, head_dim=D)
+    small = w.num_pages - w.num_pages // 4
+    sc = w.kv_scales[0]
+    kv = K.KVCache(w.k_pages[0][:small], w.v_pages[0][:small], w.num_q_heads, torch.bfloat16,
+                   None if sc is None else sc[:small].contiguous())
+    k, v, hsc = w.host_kv()
+    pool = O.KVPool(k[:small], v[:small], w.kv_dtype, None if hsc is None else hsc[:small])
+    fbt = np.array(w.full_block_table)
+    fbt[0, 3] = -1
+    fbt[1, 0] = -100000
+    assert (fbt >= small).any() and ((fbt >= 0) & (fbt < small)).any()
+    plans = oracle_plan(w)          # compiled against the whole pool
+    cap = w.max_pages_per_seq
+    vbt, vlb, nb = plan_view_arrays(plans, cap)
+    vbt[2, 0] = -3
+    seq = dev_i32(w.seq_lens)
+    for ns in (0, 3):
+        o, lse = K.selected_decode(kv, w.q_decode[0], seq, dev_i32(vbt), dev_i32(vlb),
+                                   dev_i32(nb), cap, 1.0, num_splits=ns)
+        torch.cuda.synchronize()
+        eo, el = O.selected_decode(pool, w.q_decode[0].float().cpu().numpy(), w.seq_lens, vbt,
+                                   vlb, nb, 1.0)
+        assert_close("decode O", o.cpu().numpy(), eo, O_TOL)
+        assert_close("decode LSE", lse.cpu().numpy(), el, LSE_TOL)
+        q = _window(w, 5, 77 + ns)
+        ov, lv = K.verify(kv, q, seq, dev_i32(fbt), int(w.seq_lens.max()), 1.0, num_splits=ns)
+        torch.cuda.synchronize()
+        ev, elv = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, fbt, 1.0)
+        assert_close("verify O", ov.cpu().numpy(), ev, O_TOL)
+        assert_close("verify LSE", lv.cpu().numpy(), elv, LSE_TOL)

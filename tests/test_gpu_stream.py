@@ -1,7 +1,8 @@
 """GPU run of the ragged fp8 workload's interleaved stream (proposal decode and
 gamma in {2,4,8} verify windows, geometric(0.6) accept lengths, fallback to
-full-context access) with outputs checked against the oracle: a decode step
-after fallbacks (mixed selected / full views) and the last verify window."""
+full-context access) with the access modes and outputs checked against the
+oracle: a decode step after fallbacks (mixed selected / full views) and the
+last verify window."""
 import numpy as np
 import pytest
 import torch
@@ -17,25 +18,22 @@ pytestmark = pytest.mark.gpu
 
 
 def oracle_views(w, plans, mode):
+    """The oracle's active view rows (O.active_view) for per-sequence modes."""
     B, cap = w.batch, w.fbt_stride
     vbt = np.zeros((B, cap), np.int64)
     vlb = np.zeros((B, cap), np.int64)
     nb = np.zeros(B, np.int64)
     for b, p in enumerate(plans):
-        if mode[b] == FULL:
-            n = -(-int(w.seq_lens[b]) // 16)
-            vbt[b, :n] = w.full_block_table[b, :n]
-            vlb[b, :n] = np.arange(n)
-            nb[b] = n
-        else:
-            vbt[b, :p.num_blocks] = p.block_table
-            vlb[b, :p.num_blocks] = p.logical_blocks
-            nb[b] = p.num_blocks
+        bt, lb, n, _ = O.active_view(int(mode[b]), p, w.full_block_table[b], int(w.seq_lens[b]))
+        vbt[b, :n], vlb[b, :n], nb[b] = bt, lb, n
     return vbt, vlb, nb
 
 
 def test_config5_stream_with_fallback():
-    # 16 sequences of the ragged fp8 recipe (lengths 4K..64K), 8 cycles
+    # 16 sequences of the ragged fp8 recipe (lengths 4K..64K), 8 cycles. The
+    # reference is the oracle throughout: oracle plans, the oracle's access
+    # modes per cycle from the workload's accept draws, the oracle's active
+    # views, the oracle's decode / verify.
     w = make_workload(5, device="cuda", batch=16, seq_len=65536, n_verify=8)
     kv = kv_of(w)
     plan = gpu_plan(w)
@@ -43,23 +41,36 @@ def test_config5_stream_with_fallback():
     res = run_stream(w, kv, plan, keep_outputs={("decode", i) for i in range(n_dec)} |
                      {("verify", len(w.q_verify) - 1)})
     torch.cuda.synchronize()
-    assert (res.policy.mode == FULL).any(), "the recipe's accept law should trigger fallbacks"
-    assert len(res.decode_out) == n_dec
-    # steps to check: the first, the one with the most even selected/full mix, the last
-    mixes = [abs(int((m == FULL).sum()) - w.batch // 2) for _, _, _, m in res.decode_out]
-    picks = sorted({0, int(np.argmin(mixes)), n_dec - 1})
     pool = oracle_pool(w)
     plans = O.compile_plan(w.seq_lens, w.full_block_table, w.span_offsets, w.span_start,
                            w.span_len, w.span_prior, w.prefix, w.suffix, w.budget,
                            O.SELECT_SKIP, w.num_pages, w.max_pages_per_seq)
+    gammas = [q.shape[1] - 1 for q in w.q_verify]
+    modes = O.access_modes([p.status for p in plans], [p.view_tokens for p in plans],
+                           w.seq_lens, w.accept_draws, gammas, 4)
+    # decode call i runs in cycle cycle_of[i], with the modes after the cycles before it
+    cycle_of, c = {}, 0
+    for kind, idx in w.schedule:
+        if kind == "decode":
+            cycle_of[idx] = c
+        else:
+            c += 1
+    assert np.array_equal(res.policy.mode, modes[-1])
+    assert (modes[-1] == FULL).any(), "the recipe's accept law should trigger fallbacks"
+    assert len(res.decode_out) == n_dec
+    for idx, _, _, mode_then in res.decode_out:
+        assert np.array_equal(mode_then, modes[cycle_of[idx]]), idx
+    # steps to check: the first, the one with the most even selected/full mix, the last
+    mixes = [abs(int((modes[cycle_of[i]] == FULL).sum()) - w.batch // 2) for i in range(n_dec)]
+    picks = sorted({0, int(np.argmin(mixes)), n_dec - 1})
     for k in picks:
-        idx, o, l, mode_then = res.decode_out[k]
-        vbt, vlb, nb = oracle_views(w, plans, mode_then)
+        idx, o, l, _ = res.decode_out[k]
+        vbt, vlb, nb = oracle_views(w, plans, modes[cycle_of[idx]])
         qh = w.q_decode[idx].float().cpu().numpy()
         eo, el = O.selected_decode(pool, qh, w.seq_lens, vbt, vlb, nb, w.sm_scale)
         assert_close(f"stream decode {idx} O", o.cpu().numpy(), eo, O_TOL)
         assert_close(f"stream decode {idx} LSE", l.cpu().numpy(), el, LSE_TOL)
-    mixed = res.decode_out[picks[len(picks) // 2]][3]
+    mixed = modes[cycle_of[res.decode_out[picks[len(picks) // 2]][0]]]
     assert 0 < int((mixed == FULL).sum()) < w.batch, "a checked step mixes both view kinds"
     # last verify window: sequences 0 and 7, all heads
     j, ov, lv = res.verify_out[0]
@@ -67,3 +78,23 @@ def test_config5_stream_with_fallback():
                        w.full_block_table, w.sm_scale, batches=[0, 7])
     assert_close("stream verify O", ov.cpu().numpy()[[0, 7]], ev[[0, 7]], O_TOL)
     assert_close("stream verify LSE", lv.cpu().numpy()[[0, 7]], elv[[0, 7]], LSE_TOL)
+
+
+def test_run_stream_on_a_side_stream_matches_the_current_stream():
+    # the binding allocates its temporaries (zero-filled workspaces, outputs)
+    # on the launch stream: the host-policy stream run on a side stream, with
+    # no workspace passed to verify, gives bit-identical results to the same
+    # stream on torch's current stream
+    w = make_workload(5, device="cuda", batch=8, seq_len=32768, n_verify=4)
+    kv = kv_of(w)
+    plan = gpu_plan(w)
+    keep = {("verify", j) for j in range(len(w.q_verify))} | {("decode", 0)}
+    a = run_stream(w, kv, plan, keep_outputs=keep)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    b = run_stream(w, kv, plan, keep_outputs=keep, stream=side)
+    side.synchronize()
+    assert np.array_equal(a.policy.mode, b.policy.mode)
+    for (j1, o1, l1), (j2, o2, l2) in zip(a.verify_out, b.verify_out):
+        assert j1 == j2 and torch.equal(o1, o2) and torch.equal(l1, l2), j1
+    assert torch.equal(a.decode_out[0][1], b.decode_out[0][1])
