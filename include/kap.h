@@ -21,7 +21,8 @@
  * --------------------------------
  * - Every array argument is device memory owned by the caller. The library
  *   never allocates, frees or synchronises, and keeps no pointer after the
- *   call returns. Work is enqueued on `stream` (a hipStream_t passed as
+ *   call returns (kap_selected_decode_noalloc uses a scratch buffer the
+ *   library holds per GPU instead of a workspace; see there). Work is enqueued on `stream` (a hipStream_t passed as
  *   void*; NULL = the default stream); the caller keeps every buffer alive
  *   until that work has completed.
  * - Scratch memory comes from the caller's `workspace`, at least the size the
@@ -252,6 +253,33 @@ kap_status kap_selected_decode_masked(const kap_kv_cache *kv, int32_t batch, con
                                       const int32_t *view_num_blocks, int32_t max_view_blocks,
                                       float sm_scale, int32_t num_splits, float *out, float *lse,
                                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * kap_selected_decode_noalloc -- kap_selected_decode for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc. It takes no workspace and allocates
+ * nothing: the split partials and arrival counters live in a scratch buffer
+ * the library holds on each GPU it runs on (16 MiB, kept until the process
+ * ends; its address is looked up once per device, on the first call there).
+ *
+ * Arguments, results and every other error are those of kap_selected_decode.
+ * Limits: the split partials the call needs -- what
+ * kap_selected_decode_workspace_bytes() reports for the same arguments, less
+ * its arrival-counter block -- at most 16 MiB - 64 KiB, else
+ * KAP_ERR_WORKSPACE_TOO_SMALL; with split partials on the tuned path
+ * (head_dim 128, four query heads per KV head), batch * num_kv_heads <=
+ * 16384, else KAP_ERR_UNSUPPORTED. Both are reported before anything is
+ * enqueued. The counters are zero when the library is loaded and every
+ * completed call leaves them zero. All calls on one GPU share its scratch:
+ * calls that may overlap in time on one GPU (on different streams, or from
+ * different threads) race and give wrong results; keep them stream-ordered.
+ */
+kap_status kap_selected_decode_noalloc(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                       const int32_t *seq_lens, const int32_t *view_block_table,
+                                       const int32_t *view_logical_block, int32_t view_stride,
+                                       const int32_t *view_num_blocks, int32_t max_view_blocks,
+                                       float sm_scale, int32_t num_splits, float *out, float *lse,
+                                       void *stream);
 
 /*
  * kap_verify -- full-context verification attention of the q_len = k+1

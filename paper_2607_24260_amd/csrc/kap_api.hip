@@ -241,8 +241,52 @@ size_t partial_bytes(const kap_kv_cache *kv, int batch, int q_len, const SplitPl
   return ws_layout(kv, batch, q_len, p).total;
 }
 
+// Device scratch of kap_selected_decode_noalloc: one copy per GPU, zero when
+// the library's code object is loaded there. Fixed layout: the arrival
+// counters of the fused split merge in the first kScratchTicketBytes (the
+// kernels leave every counter they use at zero), the split partials after
+// them, so that no call's partials overlap another call's counters. In host
+// code `scratch` only names the variable; its device address comes from
+// scratch_base().
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr size_t kScratchTicketBytes = size_t(64) << 10;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current); nullptr if the lookup fails.
+void *scratch_base(hipError_t *err) {
+  static std::mutex mu;
+  static void *cache[64] = {nullptr};
+  int dev = 0;
+  *err = hipGetDevice(&dev);
+  if (*err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= 64) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!cache[dev]) {
+    void *ptr = nullptr;
+    *err = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (*err != hipSuccess) return nullptr;
+    cache[dev] = ptr;
+  }
+  return cache[dev];
+}
+
+// The static scratch layout for a call whose workspace layout is w (its
+// partial o and lse blocks, moved behind the fixed counter block).
+WsLayout scratch_layout(const WsLayout &w) {
+  WsLayout f{0, 0, 0, 0};
+  if (w.total == 0) return f;
+  f.part_o = kScratchTicketBytes;
+  f.part_lse = f.part_o + (w.part_lse - w.part_o);
+  f.total = f.part_lse + (w.total - w.part_lse);
+  return f;
+}
+
 kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const SplitPlan &p,
-                            bool decode, void *ws, hipStream_t s) {
+                            bool decode, void *ws, const WsLayout &w, hipStream_t s) {
   a.n_split = p.n_split;
   a.pages_per_split = p.pps;
   a.ragged = p.ragged ? 1 : 0;
@@ -254,7 +298,7 @@ kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const Spli
     const long long ng = units > 0 ? p.w_target / units : 1;
     a.guess_splits = ng > 1 ? (int)ng : 1;
   }
-  const WsLayout w = ws_layout(kv, a.batch, a.q_len, p);
+  (void)kv;
   if (p.fast && w.total > 0x7fffffffULL)
     return fail(KAP_ERR_UNSUPPORTED, "split partials need %zu bytes (> 2 GiB); pass fewer splits",
                 w.total);
@@ -429,7 +473,7 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
                                   int32_t view_stride, const int32_t *view_num_blocks,
                                   int32_t max_view_blocks, float sm_scale, int32_t num_splits,
                                   float *out, float *lse, void *workspace,
-                                  size_t workspace_bytes, void *stream) {
+                                  size_t workspace_bytes, void *stream, bool noalloc = false) {
   kap_status st = check_kv(kv);
   if (st != KAP_OK) return st;
   if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
@@ -452,11 +496,33 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
   if (!aligned(q, 16) || !aligned(out, 16))
     return fail(KAP_ERR_INVALID_ARGUMENT, "q and out must be 16-byte aligned");
   const SplitPlan p = plan_decode(kv, batch, max_view_blocks, num_splits);
-  const size_t need = partial_bytes(kv, batch, 1, p);
-  if (need > 0 && (!workspace || workspace_bytes < need))
-    return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need, workspace_bytes);
-  if (need > 0 && !aligned(workspace, 256))
-    return fail(KAP_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  WsLayout layout = ws_layout(kv, batch, 1, p);
+  if (noalloc) {
+    // the library's own scratch instead of a workspace
+    layout = scratch_layout(layout);
+    if (p.fast && layout.total > 0 &&
+        (size_t)batch * kv->num_kv_heads * sizeof(int32_t) > kScratchTicketBytes)
+      return fail(KAP_ERR_UNSUPPORTED,
+                  "batch * num_kv_heads = %lld exceeds the %zu arrival counters of the "
+                  "allocation-free call's scratch", (long long)batch * kv->num_kv_heads,
+                  kScratchTicketBytes / sizeof(int32_t));
+    if (layout.total > kScratchBytes)
+      return fail(KAP_ERR_WORKSPACE_TOO_SMALL,
+                  "the call's split partials need %zu bytes; the allocation-free call's scratch "
+                  "holds %zu (use kap_selected_decode with a workspace)",
+                  layout.total - kScratchTicketBytes, kScratchBytes - kScratchTicketBytes);
+    hipError_t e = hipSuccess;
+    workspace = scratch_base(&e);
+    if (!workspace)
+      return fail(KAP_ERR_HIP, "device address of the scratch buffer: %s", hipGetErrorString(e));
+  } else {
+    const size_t need = layout.total;
+    if (need > 0 && (!workspace || workspace_bytes < need))
+      return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "workspace needs %zu bytes, got %zu", need,
+                  workspace_bytes);
+    if (need > 0 && !aligned(workspace, 256))
+      return fail(KAP_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  }
 
   kap::AttnArgs a;
   a.batch = batch;
@@ -488,7 +554,7 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
   a.scale_log2 = sm_scale * kap::kLog2e;
   a.out = out;
   a.lse = lse;
-  return launch_attention(a, kv, p, true, workspace, static_cast<hipStream_t>(stream));
+  return launch_attention(a, kv, p, true, workspace, layout, static_cast<hipStream_t>(stream));
 }
 
 kap_status kap_selected_decode(const kap_kv_cache *kv, int32_t batch, const void *q,
@@ -512,6 +578,17 @@ kap_status kap_selected_decode_masked(const kap_kv_cache *kv, int32_t batch, con
   return selected_decode(kv, batch, q, seq_lens, view_block_table, view_logical_block,
                          view_token_mask, true, view_stride, view_num_blocks, max_view_blocks,
                          sm_scale, num_splits, out, lse, workspace, workspace_bytes, stream);
+}
+
+kap_status kap_selected_decode_noalloc(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                       const int32_t *seq_lens, const int32_t *view_block_table,
+                                       const int32_t *view_logical_block, int32_t view_stride,
+                                       const int32_t *view_num_blocks, int32_t max_view_blocks,
+                                       float sm_scale, int32_t num_splits, float *out, float *lse,
+                                       void *stream) {
+  return selected_decode(kv, batch, q, seq_lens, view_block_table, view_logical_block, nullptr,
+                         false, view_stride, view_num_blocks, max_view_blocks, sm_scale,
+                         num_splits, out, lse, nullptr, 0, stream, true);
 }
 
 // ---------------------------------------------------------------------------
@@ -582,7 +659,8 @@ kap_status kap_verify(const kap_kv_cache *kv, int32_t batch, int32_t q_len, cons
   a.scale_log2 = sm_scale * kap::kLog2e;
   a.out = out;
   a.lse = lse;
-  return launch_attention(a, kv, p, false, workspace, static_cast<hipStream_t>(stream));
+  return launch_attention(a, kv, p, false, workspace, ws_layout(kv, batch, q_len, p),
+                          static_cast<hipStream_t>(stream));
 }
 
 // ---------------------------------------------------------------------------

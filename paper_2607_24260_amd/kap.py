@@ -46,6 +46,7 @@ PAGE = 16
 EXPORTS = (
     "kap_compile_plan", "kap_compile_plan_workspace_bytes", "kap_compile_plan_masked",
     "kap_selected_decode", "kap_selected_decode_workspace_bytes", "kap_selected_decode_masked",
+    "kap_selected_decode_noalloc",
     "kap_verify", "kap_verify_workspace_bytes",
     "kap_append_kv", "kap_compact_view", "kap_fallback_update", "kap_fallback_update_masked",
     "kap_accept_top3", "kap_accept_top3_workspace_bytes",
@@ -110,6 +111,10 @@ def load_library(path: str = LIB_PATH):
     lib.kap_selected_decode_masked.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _P, _I32, _P, _I32, _F, _I32,
         _P, _P, _P, _SZ, _P]
+    lib.kap_selected_decode_noalloc.restype = _I32
+    lib.kap_selected_decode_noalloc.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _I32, _P, _I32, _F, _I32,
+        _P, _P, _P]
     lib.kap_selected_decode_workspace_bytes.restype = _SZ
     lib.kap_selected_decode_workspace_bytes.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _I32, _I32]
@@ -514,7 +519,7 @@ def _outputs(shape, dev, out, lse):
 
 def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
                  view_num_blocks, max_view_blocks, sm_scale, num_splits, out, lse, workspace,
-                 view_token_mask, stream):
+                 view_token_mask, stream, noalloc=False):
     """Validate and marshal one kap_selected_decode[_masked] call."""
     lib = load_library()
     _dev(q, "q", kv.q_dtype, 3)
@@ -533,7 +538,7 @@ def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
             raise ValueError("view_token_mask must be shaped like the view tables")
     if seq_lens.shape[0] != B or view_num_blocks.shape[0] != B:
         raise ValueError("seq_lens / view_num_blocks must have batch entries")
-    need = selected_decode_workspace_bytes(kv, B, max_view_blocks, num_splits)
+    need = 0 if noalloc else selected_decode_workspace_bytes(kv, B, max_view_blocks, num_splits)
     with torch.cuda.stream(stream):
         out, lse = _outputs((B, kv.num_q_heads, kv.head_dim), q.device, out, lse)
         workspace, have = _workspace(need, q.device, workspace)
@@ -561,6 +566,22 @@ def selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_blo
                                     view_num_blocks, max_view_blocks, sm_scale, num_splits,
                                     out, lse, workspace, view_token_mask, stream)
     _check(fn(*args))
+    return res
+
+
+def selected_decode_noalloc(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
+                            view_num_blocks, max_view_blocks: int, sm_scale: float, *,
+                            num_splits: int = 0, out=None, lse=None, stream=None):
+    """kap_selected_decode_noalloc: selected_decode without a workspace (the
+    library's per-GPU scratch holds the split partials). Returns (out, lse);
+    outputs not passed are allocated here, on the launch stream."""
+    lib = load_library()
+    fn, args, res, _ = _decode_call(kv, q, seq_lens, view_block_table, view_logical_block,
+                                    view_num_blocks, max_view_blocks, sm_scale, num_splits,
+                                    out, lse, None, None, stream, noalloc=True)
+    del fn
+    # kap_selected_decode's arguments without (workspace, workspace_bytes)
+    _check(lib.kap_selected_decode_noalloc(*args[:-3], args[-1]))
     return res
 
 
