@@ -28,13 +28,14 @@
  * - Scratch memory comes from the caller's `workspace`, at least the size the
  *   matching kap_*_workspace_bytes() call returns for the same arguments on
  *   the current device, 256-byte aligned. kap_selected_decode and kap_verify
- *   keep arrival counters in its first round_up(4 * batch * num_kv_heads, 256)
- *   bytes: that block must be zero when the call starts, and every completed
- *   call leaves it zero again. Zero-fill a workspace once when allocating it
- *   (and again if a later call uses a larger batch * num_kv_heads); the rest
- *   of the workspace is scratch whose contents do not matter. Calls that can
- *   run concurrently must not share a workspace. kap_compile_plan's workspace
- *   has no such block.
+ *   keep arrival counters in its first round_up(64 * batch * num_kv_heads,
+ *   256) bytes: that block must be zero when the call starts, and every
+ *   completed call leaves it zero again. Zero-fill a workspace once when
+ *   allocating it (and again if a later call uses a larger batch *
+ *   num_kv_heads); the rest of the workspace is scratch whose contents do not
+ *   matter, so one workspace may serve any sequence of decode and verify calls
+ *   that fit it. Calls that can run concurrently must not share a workspace.
+ *   kap_compile_plan's workspace has no such block.
  * - Grid sizes depend only on host integers, never on device data, so the
  *   calls may be captured into a HIP graph.
  * - Host-checkable errors (null pointers, negative sizes, unsupported
@@ -265,10 +266,10 @@ kap_status kap_selected_decode_masked(const kap_kv_cache *kv, int32_t batch, con
  * Arguments, results and every other error are those of kap_selected_decode.
  * Limits: the split partials the call needs -- what
  * kap_selected_decode_workspace_bytes() reports for the same arguments, less
- * its arrival-counter block -- at most 16 MiB - 64 KiB, else
+ * its arrival-counter block -- at most 16 MiB - 256 KiB, else
  * KAP_ERR_WORKSPACE_TOO_SMALL; with split partials on the tuned path
  * (head_dim 128, four query heads per KV head), batch * num_kv_heads <=
- * 16384, else KAP_ERR_UNSUPPORTED. Both are reported before anything is
+ * 4096, else KAP_ERR_UNSUPPORTED. Both are reported before anything is
  * enqueued. The counters are zero when the library is loaded and every
  * completed call leaves them zero. All calls on one GPU share its scratch:
  * calls that may overlap in time on one GPU (on different streams, or from

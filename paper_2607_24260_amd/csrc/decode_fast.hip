@@ -194,10 +194,10 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   if constexpr (BALANCED) {
     const int ng = a.guess_splits;
     const int w = blockIdx.x;
-    const int q = div_small(w, ng);
+    const int q = div_u21(w, ng);   // w < slots < 2^21
     wi.n_split = ng;
     wi.split = w - q * ng;
-    const int bq = div_small(q, a.Hkv);
+    const int bq = div_u21(q, a.Hkv);
     wi.g = q - bq * a.Hkv;
     wi.b = min(bq, a.batch - 1);
   } else {

@@ -227,7 +227,8 @@ WsLayout ws_layout(const kap_kv_cache *kv, int batch, int q_len, const SplitPlan
     if (p.n_split <= 1) return w;
     prow = (size_t)batch * q_len * kv->num_q_heads * p.n_split;
   }
-  const size_t t = round_up((size_t)batch * kv->num_kv_heads * sizeof(int32_t), 256);
+  const size_t t = round_up(
+      (size_t)batch * kv->num_kv_heads * sizeof(int32_t) * kap::kTicketStride, 256);
   const size_t o = round_up(prow * kv->head_dim * sizeof(float), 256);
   const size_t l = round_up(prow * sizeof(float), 256);
   w.tickets = 0;
@@ -249,7 +250,7 @@ size_t partial_bytes(const kap_kv_cache *kv, int batch, int q_len, const SplitPl
 // code `scratch` only names the variable; its device address comes from
 // scratch_base().
 constexpr size_t kScratchBytes = size_t(16) << 20;
-constexpr size_t kScratchTicketBytes = size_t(64) << 10;
+constexpr size_t kScratchTicketBytes = size_t(256) << 10;
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 // Device address of `scratch` on the current device, looked up once per
@@ -293,6 +294,8 @@ kap_status launch_attention(kap::AttnArgs &a, const kap_kv_cache *kv, const Spli
   a.w_target = p.w_target;
   a.w_uneven = p.w_uneven;
   a.min_chunk = p.min_chunk;
+  a.rcp_w_target = p.w_target > 0 ? 1.0 / p.w_target : 0.0;
+  a.rcp_w_uneven = p.w_uneven > 0 ? 1.0 / p.w_uneven : 0.0;
   {
     const long long units = (long long)a.batch * a.Hkv;
     const long long ng = units > 0 ? p.w_target / units : 1;
@@ -501,11 +504,12 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
     // the library's own scratch instead of a workspace
     layout = scratch_layout(layout);
     if (p.fast && layout.total > 0 &&
-        (size_t)batch * kv->num_kv_heads * sizeof(int32_t) > kScratchTicketBytes)
+        (size_t)batch * kv->num_kv_heads * sizeof(int32_t) * kap::kTicketStride >
+            kScratchTicketBytes)
       return fail(KAP_ERR_UNSUPPORTED,
                   "batch * num_kv_heads = %lld exceeds the %zu arrival counters of the "
                   "allocation-free call's scratch", (long long)batch * kv->num_kv_heads,
-                  kScratchTicketBytes / sizeof(int32_t));
+                  kScratchTicketBytes / (sizeof(int32_t) * kap::kTicketStride));
     if (layout.total > kScratchBytes)
       return fail(KAP_ERR_WORKSPACE_TOO_SMALL,
                   "the call's split partials need %zu bytes; the allocation-free call's scratch "

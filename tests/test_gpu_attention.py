@@ -428,3 +428,60 @@ def test_out_of_pool_page_ids_contribute_no_keys(kv_dtype, D):
         ev, elv = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, fbt, 1.0)
         assert_close("verify O", ov.cpu().numpy(), ev, O_TOL)
         assert_close("verify LSE", lv.cpu().numpy(), elv, LSE_TOL)
+
+
+# --------------------------------------------------------------------------
+# the workspace contract: all zero between calls, shareable by any sequence
+# of decode and verify calls
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_shared_workspace(kv_dtype):
+    # one workspace serves decode and verify calls of the tuned kernels
+    # (balanced and uniform splits) and of the generic path in turn, so each
+    # call finds the previous calls' partials in it; after every call
+    # its arrival-counter block is zero again, and every result equals the
+    # same call's result with a fresh workspace
+    cfg = 2 if kv_dtype == "bf16" else 5
+    w, _ = workload(cfg, batch=3, seq_len=6000, n_decode=1, n_verify=1)
+    # (the same batch for every call: the counter block grows with batch * Hkv)
+    w64, _ = _ragged(cfg, 3, 6000 if cfg == 5 else 3000, [2500, 700, 37], head_dim=64)
+    kv, kv64 = kv_of(w), kv_of(w64)
+    plan = gpu_plan(w)
+    cap = w.max_pages_per_seq
+    seq = dev_i32(w.seq_lens)
+    fbt = dev_i32(w.full_block_table)
+    L = int(w.seq_lens.max())
+    qv = _window(w, 5, 11)
+    fbt64 = dev_i32(w64.full_block_table)
+    qv64 = _window(w64, 3, 12)
+    need = max(K.selected_decode_workspace_bytes(kv, 3, cap, ns) for ns in (0, 3))
+    need = max(need, *(K.verify_workspace_bytes(kv, 3, 5, L, ns) for ns in (0, 5)),
+               K.verify_workspace_bytes(kv64, 3, 3, 2500, 0))
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    # everything past the counters is scratch: start it as random bytes (words
+    # that decode as records of an earlier call included)
+    ctr = 64 * 3 * 8
+    g = torch.Generator(device="cuda").manual_seed(5)
+    ws[ctr:] = torch.randint(0, 256, (need - ctr,), generator=g, device="cuda",
+                             dtype=torch.int32).to(torch.uint8)
+    calls = [
+        ("decode auto", lambda **k: K.selected_decode(
+            kv, w.q_decode[0], seq, plan["view_block_table"], plan["view_logical_block"],
+            plan["view_num_blocks"], cap, 1.0, **k)),
+        ("verify auto", lambda **k: K.verify(kv, qv, seq, fbt, L, 1.0, **k)),
+        ("generic verify", lambda **k: K.verify(kv64, qv64, dev_i32(w64.seq_lens), fbt64, 2500,
+                                                1.0, **k)),
+        ("decode 3 splits", lambda **k: K.selected_decode(
+            kv, w.q_decode[0], seq, plan["view_block_table"], plan["view_logical_block"],
+            plan["view_num_blocks"], cap, 1.0, num_splits=3, **k)),
+        ("verify 5 splits", lambda **k: K.verify(kv, qv, seq, fbt, L, 1.0, num_splits=5, **k)),
+    ]
+    for rep in range(2):
+        for name, fn in calls:
+            o, l = fn(workspace=ws)
+            torch.cuda.synchronize()
+            assert int(torch.count_nonzero(ws[:ctr])) == 0, f"{name}: counters not zero"
+            o2, l2 = fn()
+            torch.cuda.synchronize()
+            assert torch.equal(o, o2) and torch.equal(l, l2), name

@@ -73,9 +73,9 @@ def test_calls_beyond_the_scratch_are_refused_before_launch():
     with pytest.raises(K.KapError) as e:
         K.selected_decode_noalloc(kv, q, n * 16, tab, tab, n, cap, 1.0)
     assert e.value.status == K.KAP_ERR_WORKSPACE_TOO_SMALL and "scratch" in str(e.value)
-    # tuned path, uniform splits: 2100 x 8 (sequence, KV head) units need more
+    # tuned path, uniform splits: 600 x 8 (sequence, KV head) units need more
     # arrival counters than the scratch holds
-    B = 2100
+    B = 600
     kb = torch.zeros((4, Hkv, D // 8, 16, 8), dtype=torch.bfloat16, device=dev)
     vb = torch.zeros((4, Hkv, D, 16), dtype=torch.bfloat16, device=dev)
     kvb = K.KVCache(kb, vb, Hq, torch.bfloat16)
