@@ -11,8 +11,12 @@ buffer far exceed the 256 MB Infinity Cache -- the numbers are HBM numbers.
 
 Printed: one JSON line (rank 0). `value` is effective KV GB/s of the whole
 step (algorithmic bytes / step time); decode steps/s, verify calls/s, the
-roofline of the dominant call (kap_verify) and the CPU oracle on a bounded
-sample are included. Diagnostics go to stderr.
+roofline of the dominant call (kap_verify) and of decode, and `per_config`:
+plan / decode / verify per call for every workload (1-3 timed here, 5 from its
+device-resident stream), each beside the fp64 oracle's median-of-3 call times
+on the host cores (bounded samples, scaled by KV bytes; workload 1 also on one
+thread). `cpu_baseline` is the oracle's rate on the 128K step. Diagnostics go
+to stderr.
 """
 from __future__ import annotations
 
@@ -110,48 +114,12 @@ def time_loop(fn, n, reps, torch):
     return statistics.median(out)
 
 
-def cpu_baseline(w, budget_s=12.0):
-    """The fp64 oracle on the host cores, on a bounded sample of the workload:
-    one plan compile, then the step's schedule in order (a decode call over the
-    whole batch, or a verify call over the whole batch) until `budget_s` seconds
-    of work are done. Rate = algorithmic bytes of the calls done / wall time."""
-    from oracle import kap_oracle as O
+def _host_info():
     try:
         from threadpoolctl import threadpool_info
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         blas_threads = 1
-    k, v, sc = w.host_kv(0)
-    pool = O.KVPool(k, v, w.kv_dtype, sc)
-    t0 = time.perf_counter()
-    plans = O.compile_plan(w.seq_lens, w.full_block_table, w.span_offsets, w.span_start,
-                           w.span_len, w.span_prior, w.prefix, w.suffix, w.budget, 0,
-                           w.num_pages, w.max_pages_per_seq)
-    t_plan = time.perf_counter() - t0
-    vbt = np.zeros((w.batch, w.max_pages_per_seq), np.int64)
-    vlb = np.zeros_like(vbt)
-    for b, p in enumerate(plans):
-        vbt[b, :p.num_blocks] = p.block_table
-        vlb[b, :p.num_blocks] = p.logical_blocks
-    nb = [p.num_blocks for p in plans]
-    vt = [p.view_tokens for p in plans]
-    total = plan_bytes(w, nb)
-    done = {"decode": 0, "verify": 0}
-    secs = t_plan
-    for kind, i in w.schedule:
-        t0 = time.perf_counter()
-        if kind == "decode":
-            O.selected_decode(pool, w.q_decode[i].float().cpu().numpy(), w.seq_lens, vbt, vlb,
-                              nb, w.sm_scale)
-            total += algorithmic_bytes(w, vt, nb, "decode")
-        else:
-            qv = w.q_verify[i].float().cpu().numpy()
-            O.verify(pool, qv, w.seq_lens, w.full_block_table, w.sm_scale)
-            total += algorithmic_bytes(w, vt, nb, "verify", qv.shape[1])
-        secs += time.perf_counter() - t0
-        done[kind] += 1
-        if secs >= budget_s:
-            break
     aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     model = ""
     try:
@@ -161,15 +129,94 @@ def cpu_baseline(w, budget_s=12.0):
                 break
     except OSError:
         pass
+    return {"host_cpus": os.cpu_count(), "affinity_cpus": aff, "blas_threads": int(blas_threads),
+            "cpu_model": model}
+
+
+def _median_s(fn, reps):
+    ts = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        fn()
+        ts.append(time.perf_counter() - t0)
+    return statistics.median(ts)
+
+
+def oracle_call_times(w, dec_seqs=None, ver_heads=1, reps=3):
+    """The fp64 oracle on the host cores, median of `reps` runs each, for one
+    plan compile, one decode step and one verify call of workload `w` (KV of
+    replica 0, the first decode / verify queries).
+
+    Bounded samples: decode runs over the first `dec_seqs` sequences (all when
+    None); verify over sequence 0 with KV heads 0 .. ver_heads - 1 (every
+    (sequence, KV head) unit of verify is independent and reads its own KV).
+    Each sample time is scaled to the whole call by the KV bytes it reads
+    (decode: view tokens; verify: sequence length x KV heads), and GB/s is the
+    call's algorithmic bytes over that scaled time."""
+    from oracle import kap_oracle as O
+    k, v, sc = w.host_kv(0)
+    pool = O.KVPool(k, v, w.kv_dtype, sc)
+    B, Hkv = w.batch, w.num_kv_heads
+
+    def compile_():
+        return O.compile_plan(w.seq_lens, w.full_block_table, w.span_offsets, w.span_start,
+                              w.span_len, w.span_prior, w.prefix, w.suffix, w.budget, 0,
+                              w.num_pages, w.max_pages_per_seq)
+
+    t_plan = _median_s(compile_, reps)
+    plans = compile_()
+    vbt = np.zeros((B, w.max_pages_per_seq), np.int64)
+    vlb = np.zeros_like(vbt)
+    for b, p in enumerate(plans):
+        vbt[b, :p.num_blocks] = p.block_table
+        vlb[b, :p.num_blocks] = p.logical_blocks
+    nb = np.array([p.num_blocks for p in plans], dtype=np.int64)
+    vt = np.array([p.view_tokens for p in plans], dtype=np.int64)
+
+    nd = B if dec_seqs is None else min(B, dec_seqs)
+    qd = w.q_decode[0].float().cpu().numpy()[:nd]
+    t_dec_s = _median_s(lambda: O.selected_decode(pool, qd, w.seq_lens[:nd], vbt[:nd], vlb[:nd],
+                                                  nb[:nd], w.sm_scale), reps)
+    t_dec = t_dec_s * float(vt.sum()) / max(float(vt[:nd].sum()), 1.0)
+
+    qv = w.q_verify[0].float().cpu().numpy()
+    nh = min(Hkv, ver_heads)
+    t_ver_s = _median_s(lambda: O.verify(pool, qv, w.seq_lens, w.full_block_table, w.sm_scale,
+                                         batches=[0], kv_heads=range(nh)), reps)
+    L = np.asarray(w.seq_lens, dtype=np.float64)
+    t_ver = t_ver_s * float(L.sum()) * Hkv / (float(L[0]) * nh)
+
+    dec_b = algorithmic_bytes(w, vt, nb, "decode")
+    ver_b = algorithmic_bytes(w, vt, nb, "verify", qv.shape[1])
     return {
-        "value": round(total / secs / 1e9, 4), "unit": "GB/s", "cores": int(blas_threads),
+        "compile_s": round(t_plan, 4),
+        "decode_call_s": round(t_dec, 4), "decode_sample_s": round(t_dec_s, 4),
+        "decode_sample": f"{nd} of {B} sequences, all {Hkv} KV heads",
+        "decode_gbs": round(dec_b / t_dec / 1e9, 4),
+        "verify_call_s": round(t_ver, 4), "verify_sample_s": round(t_ver_s, 4),
+        "verify_sample": f"sequence 0 ({int(L[0])} tokens), {nh} of {Hkv} KV heads, "
+                         f"q_len {qv.shape[1]}",
+        "verify_gbs": round(ver_b / t_ver / 1e9, 4),
+        "reps": reps,
+    }
+
+
+def cpu_baseline(w, n_dec, n_ver, step_b, oracle):
+    """The oracle's rate on the bench step of workload `w` (1 compile, n_dec
+    decode and n_ver verify calls), from the per-call medians of
+    oracle_call_times: algorithmic bytes of the step / the oracle's time for
+    it."""
+    t_step = oracle["compile_s"] + n_dec * oracle["decode_call_s"] + n_ver * oracle["verify_call_s"]
+    info = _host_info()
+    return {
+        "value": round(step_b / t_step / 1e9, 4), "unit": "GB/s", "cores": info["blas_threads"],
         "kind": "oracle",
-        "sample": (f"1 plan compile ({t_plan:.2f}s), then the step's schedule in order until "
-                   f"{budget_s:.0f}s: {done['decode']} decode calls and {done['verify']} verify "
-                   f"calls over all {w.batch} sequences; fp64 numpy"),
-        "seconds": round(secs, 3),
-        "host_cpus": os.cpu_count(), "affinity_cpus": aff, "blas_threads": blas_threads,
-        "cpu_model": model,
+        "sample": (f"median of {oracle['reps']} runs each of 1 plan compile, 1 decode step "
+                   f"({oracle['decode_sample']}) and 1 verify call ({oracle['verify_sample']}), "
+                   f"each scaled to its whole call by KV bytes, combined as the step's "
+                   f"1 + {n_dec} + {n_ver} calls; fp64 numpy"),
+        "seconds_step_estimate": round(t_step, 3),
+        **info,
     }
 
 
@@ -233,6 +280,106 @@ def _attention_calls(torch, K, w, R, dev):
     return t_view, t_full, t_ver, s
 
 
+def config_figures(torch, K, dev, cfg, with_cpu):
+    """GPU figures of workload `cfg` (1-3) with the oracle beside them: plan
+    compile, selected-view decode and verify per call (decode and verify
+    rotating over R KV replicas, R x the decode call's KV >= 1 GiB); for
+    workload 3 also its all-blocks plan (budget = L and one span over the
+    whole sequence, so the view is the full block table) and the decode over
+    it, which is full-context decode."""
+    from paper_2607_24260_amd.workloads import DESCRIPTIONS, make_workload
+    R = {1: 32, 2: 14, 3: 5}[cfg]
+    w = make_workload(cfg, device=dev, replicas=R)
+    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32)).to(dev)
+    B, Hq, D, cap = w.batch, w.num_q_heads, w.head_dim, w.max_pages_per_seq
+    qdt = torch.float32 if w.q_dtype == "f32" else torch.bfloat16
+    kvs = [K.KVCache(w.k_pages[r], w.v_pages[r], Hq, qdt, w.kv_scales[r]) for r in range(R)]
+    seq_lens, fbt = i32(w.seq_lens), i32(w.full_block_table)
+    Lmax = int(w.seq_lens.max())
+    q_len = w.q_verify[0].shape[1]
+    nq, nv = w.q_decode.shape[0], len(w.q_verify)
+
+    def plan_for(span_offsets, span_start, span_len, prior, budget):
+        out = {
+            "view_block_table": torch.zeros((B, cap), dtype=torch.int32, device=dev),
+            "view_logical_block": torch.zeros((B, cap), dtype=torch.int32, device=dev),
+            "view_num_blocks": torch.zeros(B, dtype=torch.int32, device=dev),
+            "view_tokens": torch.zeros(B, dtype=torch.int32, device=dev),
+            "spans_taken": torch.zeros(B, dtype=torch.int32, device=dev),
+            "plan_status": torch.zeros(B, dtype=torch.int32, device=dev),
+            "span_selected": torch.zeros(len(span_start), dtype=torch.int32, device=dev),
+        }
+        ws = torch.empty(max(K.compile_plan_workspace_bytes(B, len(span_start), w.fbt_stride),
+                             256), dtype=torch.uint8, device=dev)
+        call = K.bind_compile_plan(seq_lens, fbt, i32(span_offsets), i32(span_start),
+                                   i32(span_len), torch.as_tensor(prior).to(dev), i32(w.prefix),
+                                   i32(w.suffix), i32(budget), num_pages=w.num_pages,
+                                   view_capacity=cap, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.all(out["plan_status"].cpu().numpy() == 0)
+        t = time_loop(lambda i: call(), 50, 3, torch)
+        return out, t
+
+    def decode_figures(plan):
+        vt = plan["view_tokens"].cpu().numpy()
+        vb = plan["view_num_blocks"].cpu().numpy()
+        o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        l = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        ws = torch.zeros(max(256, K.selected_decode_workspace_bytes(kvs[0], B, cap)),
+                         dtype=torch.uint8, device=dev)
+        calls = [[K.bind_selected_decode(kvs[r], w.q_decode[s], seq_lens,
+                                         plan["view_block_table"], plan["view_logical_block"],
+                                         plan["view_num_blocks"], cap, w.sm_scale, o, l, ws)
+                  for s in range(nq)] for r in range(R)]
+        t = time_loop(lambda i: calls[i % R][i % nq](), max(200, 3 * R), 5, torch)
+        nbytes = algorithmic_bytes(w, vt, vb, "decode")
+        gbs = nbytes / (t * 1e-3) / 1e9
+        return {"us_per_call": round(t * 1e3, 3), "steps_per_s": round(1e3 / t, 1),
+                "effective_gbs": round(gbs, 1), "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                "algorithmic_bytes": nbytes, "view_tokens": int(vt.sum()),
+                "retained_ratio_s_mean": round(float(np.mean(vt / w.seq_lens)), 4)}
+
+    plan, t_plan = plan_for(w.span_offsets, w.span_start, w.span_len, w.span_prior, w.budget)
+    dec = decode_figures(plan)
+    ov = torch.empty((B, q_len, Hq, D), dtype=torch.float32, device=dev)
+    lv = torch.empty((B, q_len, Hq), dtype=torch.float32, device=dev)
+    ws_v = torch.zeros(max(256, K.verify_workspace_bytes(kvs[0], B, q_len, Lmax)),
+                       dtype=torch.uint8, device=dev)
+    ver_calls = [[K.bind_verify(kvs[r], w.q_verify[j], seq_lens, fbt, Lmax, w.sm_scale, ov, lv,
+                                ws_v) for j in range(nv)] for r in range(R)]
+    t_ver = time_loop(lambda i: ver_calls[i % R][i % nv](), max(24, 3 * R), 3, torch)
+    ver_b = algorithmic_bytes(w, None, None, "verify", q_len)
+    ver_gbs = ver_b / (t_ver * 1e-3) / 1e9
+    out = {
+        "workload": f"config{cfg}: {DESCRIPTIONS[cfg]}", "kv_replicas": R,
+        "kv_dtype": w.kv_dtype, "q_dtype": w.q_dtype,
+        "plan_us_per_call": round(t_plan * 1e3, 2),
+        "decode": dec,
+        "verify": {"us_per_call": round(t_ver * 1e3, 2), "q_len": q_len,
+                   "effective_gbs": round(ver_gbs, 1),
+                   "pct_hbm_peak": round(100 * ver_gbs / HBM_PEAK_GBS, 2),
+                   "algorithmic_bytes": ver_b},
+    }
+    if cfg == 3:
+        offs = np.arange(B + 1, dtype=np.int32)
+        full, t_full_plan = plan_for(offs, np.zeros(B, np.int32), w.seq_lens,
+                                     np.ones(B, np.float32), w.seq_lens)
+        assert torch.equal(full["view_num_blocks"].cpu(),
+                           torch.as_tensor(-(-np.asarray(w.seq_lens, np.int64) // 16)).int())
+        out["all_blocks_plan"] = {"plan_us_per_call": round(t_full_plan * 1e3, 2),
+                                  "decode": decode_figures(full)}
+    if with_cpu:
+        out["oracle"] = oracle_call_times(w, ver_heads=1 if cfg > 1 else w.num_kv_heads)
+        if cfg == 1:
+            from threadpoolctl import threadpool_limits
+            with threadpool_limits(limits=1):
+                out["oracle_1_thread"] = oracle_call_times(w, ver_heads=w.num_kv_heads)
+    log(f"config {cfg}: {out}")
+    del w, kvs
+    torch.cuda.empty_cache()
+    return out
+
+
 def rq1_sweep(torch, K, dev):
     """Kernel-level analog of the paper's Table 2: B = 4 sequences per context
     bucket with the bucket's retained ratio s as the budget; selected-view
@@ -287,7 +434,7 @@ def tp4_share(torch, K, dev):
     return out
 
 
-def ragged_stream(torch, K, dev, reps=3):
+def ragged_stream(torch, K, dev, reps=3, with_cpu=False):
     """The ragged fp8 workload (64 sequences of 4K..128K tokens, fp8 KV with
     per-page scales, budgets 3%..30%) run device-resident, as
     executor.DeviceStream runs it: one plan compile, then 16 cycles of gamma in
@@ -335,18 +482,20 @@ def ragged_stream(torch, K, dev, reps=3):
 
     # algorithmic bytes of one stream, following the (identical) host policy
     policy = FallbackPolicy(vtok / L, status == K.KAP_PLAN_OK)
-    nbytes, n_dec, n_ver = plan_bytes(w, vblk), 0, 0
+    dec_bytes = ver_bytes = n_dec = n_ver = 0
     for kind, idx in w.schedule:
         if kind == "decode":
             full = policy.mode == FULL
             tok = np.where(full, L, vtok)
             pages = np.where(full, pages_full, vblk)
-            nbytes += int(tok.sum()) * 2048 + int(pages.sum()) * 16 + B * 8 + B * Hq * (D * 6 + 4)
+            dec_bytes += (int(tok.sum()) * 2048 + int(pages.sum()) * 16 + B * 8
+                          + B * Hq * (D * 6 + 4))
             n_dec += 1
         else:
-            nbytes += algorithmic_bytes(w, None, None, "verify", gammas[idx] + 1)
+            ver_bytes += algorithmic_bytes(w, None, None, "verify", gammas[idx] + 1)
             policy.update(accepted_counts(w.accept_draws[idx], gammas[idx]), gammas[idx])
             n_ver += 1
+    nbytes = plan_bytes(w, vblk) + dec_bytes + ver_bytes
     flips = int((policy.mode == FULL).sum())
 
     def timed(launch, stream):
@@ -392,6 +541,11 @@ def ragged_stream(torch, K, dev, reps=3):
         dt[kind] += prev.elapsed_time(e)
         prev = e
     gbs = nbytes / (ms_graph * 1e-3) / 1e9
+    dec_gbs = dec_bytes / (dt["decode"] * 1e-3) / 1e9
+    ver_gbs = ver_bytes / (dt["verify"] * 1e-3) / 1e9
+    oracle = None
+    if with_cpu:
+        oracle = oracle_call_times(w, dec_seqs=2, ver_heads=1)
     return {
         "workload": f"config5: {DESCRIPTIONS[5]}",
         "ms_per_stream_graph": round(ms_graph, 3), "ms_per_stream_eager": round(ms_eager, 3),
@@ -400,6 +554,11 @@ def ragged_stream(torch, K, dev, reps=3):
         "decode_calls": n_dec, "verify_calls": n_ver,
         "decode_us_mean": round(1e3 * dt["decode"] / max(n_dec, 1), 2),
         "verify_us_mean": round(1e3 * dt["verify"] / max(n_ver, 1), 2),
+        "decode_effective_gbs": round(dec_gbs, 1),
+        "decode_pct_hbm_peak": round(100 * dec_gbs / HBM_PEAK_GBS, 2),
+        "verify_effective_gbs": round(ver_gbs, 1),
+        "verify_pct_hbm_peak": round(100 * ver_gbs / HBM_PEAK_GBS, 2),
+        "oracle": oracle,
         "sequences_on_full_context_at_end": flips,
         "kv_dtype": "fp8-e4m3fn + per-page fp32 scales",
         "note": "device-resident stream (plan compile, decode/verify calls, device-side "
@@ -419,6 +578,8 @@ def main():
                     help="skip the ragged fp8 stream measurement")
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the stream-read ceiling, the context sweep and the TP-share run")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-call figures of workloads 1-3")
     ap.add_argument("--profile", action="store_true",
                     help="only the timed steps (for rocprofv3 runs)")
     ap.add_argument("--ragged-only", action="store_true",
@@ -722,15 +883,39 @@ def main():
         share = tp4_share(torch, K, dev)
         log(f"tp4 share: {share}")
 
+    others = {}
+    if cfg == 4 and not args.no_configs:
+        for c in (1, 2, 3):
+            others[f"config{c}"] = config_figures(torch, K, dev, c, not args.no_cpu)
+
     ragged = None
     if not args.no_ragged and cfg == 4:
-        ragged = ragged_stream(torch, K, dev)
+        ragged = ragged_stream(torch, K, dev, with_cpu=not args.no_cpu)
         log(f"ragged fp8 stream: {ragged}")
 
-    cpu = None
+    cpu = oracle = None
     if not args.no_cpu:
-        cpu = cpu_baseline(w)
+        oracle = oracle_call_times(w, ver_heads=1)
+        cpu = cpu_baseline(w, n_dec, n_ver, step_b, oracle)
         log(f"cpu oracle: {cpu}")
+    per_config = None
+    if others:
+        per_config = {**others, f"config{cfg}": {
+            "workload": f"config{cfg}: {DESCRIPTIONS[cfg]}", "kv_replicas": R,
+            "plan_us_per_call": round(t_plan * 1e3, 2),
+            "decode": {"us_per_call": round(t_dec * 1e3, 3), "steps_per_s": round(1e3 / t_dec, 1),
+                       "effective_gbs": round(dec_gbs, 1),
+                       "pct_hbm_peak": round(100 * dec_gbs / HBM_PEAK_GBS, 2),
+                       "algorithmic_bytes": dec_b},
+            "verify": {"us_per_call": round(t_ver * 1e3, 2), "q_len": q_len,
+                       "effective_gbs": round(ver_gbs, 1),
+                       "pct_hbm_peak": round(100 * ver_gbs / HBM_PEAK_GBS, 2),
+                       "algorithmic_bytes": ver_b},
+            "oracle": oracle}}
+        if ragged is not None:
+            per_config["config5"] = {k: ragged[k] for k in (
+                "workload", "decode_us_mean", "decode_effective_gbs", "decode_pct_hbm_peak",
+                "verify_us_mean", "verify_effective_gbs", "verify_pct_hbm_peak", "oracle")}
 
     res = {
         "metric": METRIC,
@@ -793,6 +978,7 @@ def main():
         "accept_top3": accept,
         "phase_cost_model": phase,
         "ragged_fp8_stream": ragged,
+        "per_config": per_config,
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
