@@ -434,6 +434,44 @@ def tp4_share(torch, K, dev):
     return out
 
 
+def verify_windows(torch, K, dev, windows=(3, 5, 9, 13, 16), calls=12):
+    """kap_verify alone on the ragged fp8 workload's KV (64 sequences of 4K..128K
+    tokens, fp8 E4M3FN with per-page scales; the pool far exceeds the
+    Infinity Cache) for each verify window size: the gamma = 2, 4, 8 windows
+    of that workload and the largest the tuned kernel takes. Each window size
+    runs its own kernel instance (row tiles of 16 = 4 heads x 4 tokens)."""
+    from paper_2607_24260_amd.workloads import make_workload
+    w = make_workload(5, device=dev, n_decode=1, n_verify=1)
+    B, Hq, D = w.batch, w.num_q_heads, w.head_dim
+    kv = K.KVCache(w.k_pages[0], w.v_pages[0], Hq, torch.bfloat16, w.kv_scales[0])
+    seq_lens = torch.as_tensor(np.asarray(w.seq_lens, dtype=np.int32)).to(dev)
+    fbt = torch.as_tensor(np.asarray(w.full_block_table, dtype=np.int32)).to(dev)
+    Lmax = int(w.seq_lens.max())
+    pages = -(-np.asarray(w.seq_lens, dtype=np.int64) // 16)
+    pairs = int(np.sum(-(-pages // 2))) * w.num_kv_heads
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(20261202)
+    out = {"workload": "config5 KV (64 ragged sequences, fp8 E4M3FN + per-page scales)",
+           "page_pairs_per_call": pairs, "windows": []}
+    for ql in windows:
+        q = (torch.randn((B, ql, Hq, D), generator=gen, device=dev) / math.sqrt(D)).to(torch.bfloat16)
+        o = torch.empty((B, ql, Hq, D), dtype=torch.float32, device=dev)
+        l = torch.empty((B, ql, Hq), dtype=torch.float32, device=dev)
+        ws = torch.zeros(max(256, K.verify_workspace_bytes(kv, B, ql, Lmax)), dtype=torch.uint8,
+                         device=dev)
+        call = K.bind_verify(kv, q, seq_lens, fbt, Lmax, w.sm_scale, o, l, ws)
+        t = time_loop(lambda i: call(), calls, 3, torch)
+        nbytes = algorithmic_bytes(w, None, None, "verify", ql)
+        gbs = nbytes / (t * 1e-3) / 1e9
+        out["windows"].append({"q_len": ql, "row_tiles": (4 * ql + 15) // 16,
+                               "us_per_call": round(t * 1e3, 2), "effective_gbs": round(gbs, 1),
+                               "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2)})
+        log(f"fp8 verify window {ql}: {out['windows'][-1]}")
+    del w, kv
+    torch.cuda.empty_cache()
+    return out
+
+
 def ragged_stream(torch, K, dev, reps=3, with_cpu=False):
     """The ragged fp8 workload (64 sequences of 4K..128K tokens, fp8 KV with
     per-page scales, budgets 3%..30%) run device-resident, as
@@ -585,6 +623,9 @@ def main():
     ap.add_argument("--ragged-only", action="store_true",
                     help="only the ragged fp8 stream (for rocprofv3 runs of that workload); "
                          "prints its JSON object")
+    ap.add_argument("--verify-windows-only", action="store_true",
+                    help="only fp8 verify per window size on the ragged workload's KV (for "
+                         "rocprofv3 runs); prints its JSON object")
     ap.add_argument("--calibrate", action="store_true",
                     help="also run a 1 GiB device-to-device copy (known bytes for scaling "
                          "FETCH_SIZE / WRITE_SIZE counters)")
@@ -602,6 +643,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.ragged_only:
         print(json.dumps(ragged_stream(torch, K, dev)), flush=True)
+        return
+    if args.verify_windows_only:
+        print(json.dumps(verify_windows(torch, K, dev)), flush=True)
         return
     cfg = args.config
     if cfg == 5:
@@ -888,6 +932,10 @@ def main():
         for c in (1, 2, 3):
             others[f"config{c}"] = config_figures(torch, K, dev, c, not args.no_cpu)
 
+    windows = None
+    if not args.no_ragged and cfg == 4:
+        windows = verify_windows(torch, K, dev)
+
     ragged = None
     if not args.no_ragged and cfg == 4:
         ragged = ragged_stream(torch, K, dev, with_cpu=not args.no_cpu)
@@ -978,6 +1026,7 @@ def main():
         "accept_top3": accept,
         "phase_cost_model": phase,
         "ragged_fp8_stream": ragged,
+        "fp8_verify_windows": windows,
         "per_config": per_config,
         "cpu_baseline": cpu,
     }

@@ -145,10 +145,12 @@ __device__ __forceinline__ void vt_tiles(const u32x4 rows[2], uint32_t out[8]) {
 // Pair at pages k, k+1 (k + 1 may lie past the sequence) with physical ids
 // pa, pb (pb < 0 if there is no page k + 1). Missing or invalid pages, and
 // pairs past the wavefront's share (live == false), load through a zero-byte
-// descriptor: zeros, no memory traffic, and no branches.
+// descriptor: zeros, no memory traffic, and no branches. The K half (page
+// ids, K tiles, fp8 scales) and the V half (V tiles, from the page ids the K
+// half set) can be issued at different times.
 template <int KV>
-__device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, int pa, int pb,
-                                          int g, int n, int j, bool live) {
+__device__ __forceinline__ void load_pair_k(PairRegs<KV> &r, const AttnArgs &a, int pa, int pb,
+                                            int g, int n, int j, bool live) {
   r.okA = live && pa >= 0 && (int64_t)pa < a.num_pages;
   r.okB = live && pb >= 0 && (int64_t)pb < a.num_pages;
   r.pA = r.okA ? pa : 0;
@@ -157,13 +159,23 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, in
   const int ba = r.okA ? (int)tile : 0, bb = r.okB ? (int)tile : 0;
   const auto kra = tile_rsrc(a.k_pages, ((size_t)r.pA * a.Hkv + g) * tile, ba);
   const auto krb = tile_rsrc(a.k_pages, ((size_t)r.pB * a.Hkv + g) * tile, bb);
-  const auto vra = tile_rsrc(a.v_pages, ((size_t)r.pA * a.Hkv + g) * tile, ba);
-  const auto vrb = tile_rsrc(a.v_pages, ((size_t)r.pB * a.Hkv + g) * tile, bb);
 #pragma unroll
   for (int kb = 0; kb < 4; ++kb) {
     r.kA[kb] = load_k(kra, n, j, kb, r.kA[kb]);
     r.kB[kb] = load_k(krb, n, j, kb, r.kB[kb]);
   }
+  if constexpr (KV == kFP8) {
+    r.scA = page_scales(a.kv_scales, r.pA, r.okA);
+    r.scB = page_scales(a.kv_scales, r.pB, r.okB);
+  }
+}
+template <int KV>
+__device__ __forceinline__ void load_pair_v(PairRegs<KV> &r, const AttnArgs &a, int g, int n,
+                                            int j) {
+  const size_t tile = kTileBytes(KV);
+  const int ba = r.okA ? (int)tile : 0, bb = r.okB ? (int)tile : 0;
+  const auto vra = tile_rsrc(a.v_pages, ((size_t)r.pA * a.Hkv + g) * tile, ba);
+  const auto vrb = tile_rsrc(a.v_pages, ((size_t)r.pB * a.Hkv + g) * tile, bb);
   if constexpr (KV == kBF16) {
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
@@ -177,10 +189,12 @@ __device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, in
       r.vB[c] = tile_load16(vrb, c * 1024 + (16 * j + n) * 16);
     }
   }
-  if constexpr (KV == kFP8) {
-    r.scA = page_scales(a.kv_scales, r.pA, r.okA);
-    r.scB = page_scales(a.kv_scales, r.pB, r.okB);
-  }
+}
+template <int KV>
+__device__ __forceinline__ void load_pair(PairRegs<KV> &r, const AttnArgs &a, int pa, int pb,
+                                          int g, int n, int j, bool live) {
+  load_pair_k<KV>(r, a, pa, pb, g, n, j, live);
+  load_pair_v<KV>(r, a, g, n, j);
 }
 
 constexpr int kVerifyWaves = 4;
@@ -285,8 +299,12 @@ void verify_mfma_kernel(AttnArgs a) {
   // unrolled: while one pair is processed the loads of the next ones are in
   // flight. Past the end of this wavefront's pairs the loads go through an
   // empty descriptor (no traffic), so the steady state is straight-line code.
-  auto process = [&](PairRegs<KV> &P, int k) {
-
+  // next_k / next_v issue the loads of the wavefront's next pair into the
+  // registers of P as soon as this pair no longer needs them: the K half
+  // (with the fp8 scales) once the logits are computed, the V half once V
+  // has been taken out of them. With one pair buffer per wavefront this
+  // keeps the next pair's loads in flight during most of this pair's work.
+  auto process = [&](PairRegs<KV> &P, int k, auto &&next_k, auto &&next_v) {
     float kscA = a.scale_log2, kscB = a.scale_log2, vscA = 1.f, vscB = 1.f;
     if constexpr (KV == kFP8) {
       kscA *= P.scA.x;
@@ -294,39 +312,42 @@ void verify_mfma_kernel(AttnArgs a) {
       kscB *= P.scB.x;
       vscB = P.scB.y;
     }
-    // V^T pieces of lane (j, n): keys 4j .. 4j+3 of dims 16 dt + n, raw
+    const bool okA = P.okA, okB = P.okB;
+    // V^T pieces of lane (j, n): keys 4j .. 4j+3 of dims 16 dt + n, raw. bf16
+    // takes them from the registers here; fp8 rearranges them after the
+    // softmax, which frees the raw registers for the next pair's V loads.
     using VPiece = typename std::conditional<KV == kBF16, u32x2, uint32_t>::type;
     VPiece vA[8], vB[8];
+    // keys at or beyond L hold no data: zero their V so 0 * garbage cannot
+    // occur (on the raw registers: bytes of fp8 codes, halves of bf16 pairs)
+    auto zero_past_end = [&] {
+      if ((k + 2) * kPage > L) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bool zA = k * kPage + 4 * j + e >= L;
+          const bool zB = (k + 1) * kPage + 4 * j + e >= L;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) {
+            if constexpr (KV == kFP8) {
+              const uint32_t mask = ~(0xFFu << (8 * e));
+              if (zA) vA[dt] &= mask;
+              if (zB) vB[dt] &= mask;
+            } else {
+              const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
+              if (zA) vA[dt][e >> 1] &= mask;
+              if (zB) vB[dt][e >> 1] &= mask;
+            }
+          }
+        }
+      }
+    };
     if constexpr (KV == kBF16) {
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
         vA[dt] = P.vA[dt];
         vB[dt] = P.vB[dt];
       }
-    } else {
-      vt_tiles(P.vA, vA);
-      vt_tiles(P.vB, vB);
-    }
-    // keys at or beyond L hold no data: zero their V so 0 * garbage cannot
-    // occur (on the raw registers: bytes of fp8 codes, halves of bf16 pairs)
-    if ((k + 2) * kPage > L) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const bool zA = k * kPage + 4 * j + e >= L;
-        const bool zB = (k + 1) * kPage + 4 * j + e >= L;
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) {
-          if constexpr (KV == kFP8) {
-            const uint32_t mask = ~(0xFFu << (8 * e));
-            if (zA) vA[dt] &= mask;
-            if (zB) vB[dt] &= mask;
-          } else {
-            const uint32_t mask = (e & 1) ? 0x0000ffffu : 0xffff0000u;
-            if (zA) vA[dt][e >> 1] &= mask;
-            if (zB) vB[dt][e >> 1] &= mask;
-          }
-        }
-      }
+      zero_past_end();
     }
 
     // ---- S^T = K Q^T (K operands widened at use) ---------------------------------
@@ -345,8 +366,9 @@ void verify_mfma_kernel(AttnArgs a) {
         sB[nt] = mfma(kB, qop[nt][kb], sB[nt]);
       }
     }
+    next_k();
 
-    const bool needs_mask = !P.okA || !P.okB || (k + 2) > last_full;
+    const bool needs_mask = !okA || !okB || (k + 2) > last_full;
     u32x4 phi[NT], plo[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -361,8 +383,8 @@ void verify_mfma_kernel(AttnArgs a) {
         for (int e = 0; e < 4; ++e) {
           const int posA = k * kPage + 4 * j + e;
           const int posB = (k + 1) * kPage + 4 * j + e;
-          if (!P.okA || posA >= lim[nt]) z[e] = -INFINITY;
-          if (!P.okB || posB >= lim[nt]) z[4 + e] = -INFINITY;
+          if (!okA || posA >= lim[nt]) z[e] = -INFINITY;
+          if (!okB || posB >= lim[nt]) z[4 + e] = -INFINITY;
         }
       }
       float mx = z[0];
@@ -396,6 +418,12 @@ void verify_mfma_kernel(AttnArgs a) {
                       pack_bf16_exact(pl[4], pl[5]), pack_bf16_exact(pl[6], pl[7])};
     }
 
+    if constexpr (KV == kFP8) {
+      vt_tiles(P.vA, vA);
+      vt_tiles(P.vB, vB);
+      next_v();
+      zero_past_end();
+    }
     // ---- O^T += V^T P^T -----------------------------------------------------------
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
@@ -407,6 +435,7 @@ void verify_mfma_kernel(AttnArgs a) {
         acc[nt][dt] = mfma(vop, plo[nt], acc[nt][dt]);
       }
     }
+    if constexpr (KV == kBF16) next_v();
   };
 
   const int qw = q0 + wave;
@@ -433,14 +462,30 @@ void verify_mfma_kernel(AttnArgs a) {
       ahead[jr] = table_ahead(rt, voff, kpair(jr + RING));
       __builtin_amdgcn_sched_barrier(0);
     }
-    for (int i = 0; i < n_my; i += RING) {
+    auto none = [] {};
+    if constexpr (RING == 1 && KV == kFP8) {
+      // one buffer: the next pair's K and V halves are issued inside process
+      for (int i = 0; i < n_my; ++i) {
+        const int k = kpair(i + 1);
+        const int pa = lane_value(ahead[0], 0), pb = second(k, lane_value(ahead[0], 1));
+        process(
+            rr[0], kpair(i),
+            [&] { load_pair_k<KV>(rr[0], a, pa, pb, g, n, j, i + 1 < n_my); },
+            [&] {
+              load_pair_v<KV>(rr[0], a, g, n, j);
+              ahead[0] = table_ahead(rt, voff, kpair(i + 2));
+            });
+      }
+    } else {
+      for (int i = 0; i < n_my; i += RING) {
 #pragma unroll
-      for (int jr = 0; jr < RING; ++jr) {
-        if (i + jr < n_my) process(rr[jr], kpair(i + jr));
-        const int k = kpair(i + jr + RING);
-        load_pair<KV>(rr[jr], a, lane_value(ahead[jr], 0), second(k, lane_value(ahead[jr], 1)), g,
-                      n, j, i + jr + RING < n_my);
-        ahead[jr] = table_ahead(rt, voff, kpair(i + jr + 2 * RING));
+        for (int jr = 0; jr < RING; ++jr) {
+          if (i + jr < n_my) process(rr[jr], kpair(i + jr), none, none);
+          const int k = kpair(i + jr + RING);
+          load_pair<KV>(rr[jr], a, lane_value(ahead[jr], 0), second(k, lane_value(ahead[jr], 1)),
+                        g, n, j, i + jr + RING < n_my);
+          ahead[jr] = table_ahead(rt, voff, kpair(i + jr + 2 * RING));
+        }
       }
     }
   }
