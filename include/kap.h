@@ -36,6 +36,8 @@
  *   matter, so one workspace may serve any sequence of decode and verify calls
  *   that fit it. Calls that can run concurrently must not share a workspace.
  *   kap_compile_plan's workspace has no such block.
+ * - Alignment: k_pages and v_pages, and the q and out arrays of decode and
+ *   verify, must be 16-byte aligned (KAP_ERR_INVALID_ARGUMENT otherwise).
  * - Grid sizes depend only on host integers, never on device data, so the
  *   calls may be captured into a HIP graph.
  * - Host-checkable errors (null pointers, negative sizes, unsupported

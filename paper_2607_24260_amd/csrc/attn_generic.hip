@@ -11,15 +11,43 @@
 namespace kap {
 namespace {
 
+// Eight consecutive stored elements starting at element idx (a multiple of
+// 4, so every load below is aligned), widened to float: one K chunk of one
+// token, or with n4 = 1 the first four only (four tokens of one V row).
 template <int KV>
-__device__ __forceinline__ float load_elem(const void *base, size_t idx) {
+__device__ __forceinline__ void load8(const void *base, size_t idx, float out[8], bool n4 = false) {
   if constexpr (KV == kF32) {
-    return static_cast<const float *>(base)[idx];
+    const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + idx);
+    const float4 x = p[0];
+    out[0] = x.x; out[1] = x.y; out[2] = x.z; out[3] = x.w;
+    if (!n4) {
+      const float4 y = p[1];
+      out[4] = y.x; out[5] = y.y; out[6] = y.z; out[7] = y.w;
+    }
   } else if constexpr (KV == kBF16) {
-    const uint16_t h = static_cast<const uint16_t *>(base)[idx];
-    return __uint_as_float(static_cast<uint32_t>(h) << 16);
+    const uint16_t *h = static_cast<const uint16_t *>(base) + idx;
+    uint32_t w[4];
+    const uint2 x = *reinterpret_cast<const uint2 *>(h);
+    w[0] = x.x; w[1] = x.y;
+    if (!n4) {
+      const uint2 y = *reinterpret_cast<const uint2 *>(h + 4);
+      w[2] = y.x; w[3] = y.y;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (n4 && e >= 2) break;
+      out[2 * e] = __uint_as_float(w[e] << 16);
+      out[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
   } else {
-    return fp8_to_f32(static_cast<const uint8_t *>(base)[idx]);
+    const uint8_t *c = static_cast<const uint8_t *>(base) + idx;
+    const uint32_t x = *reinterpret_cast<const uint32_t *>(c);
+    const uint32_t y = n4 ? 0u : *reinterpret_cast<const uint32_t *>(c + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[e] = fp8_to_f32((uint8_t)(x >> (8 * e)));
+      out[4 + e] = fp8_to_f32((uint8_t)(y >> (8 * e)));
+    }
   }
 }
 
@@ -71,12 +99,15 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(AttnArgs a) {
         !a.token_mask || ((a.token_mask[(size_t)b * a.bt_stride + k] >> tok) & 1u);
     float z = -INFINITY;
     if (shown && page >= 0 && page < a.num_pages && pos < limit && pos < L) {
-      // K page tile: [D/8 chunks][16 tokens][8 dims]
+      // K page tile: [D/8 chunks][16 tokens][8 dims]; one chunk per load
       const size_t kbase = ((size_t)page * a.Hkv + g) * kPage * D + (size_t)tok * 8;
       float acc = 0.f;
-      for (int d = 0; d < D; ++d)
-        acc = fmaf(qs[d], load_elem<KV>(a.k_pages, kbase + (size_t)(d >> 3) * (kPage * 8) + (d & 7)),
-                   acc);
+      for (int c = 0; c < D / 8; ++c) {
+        float kc[8];
+        load8<KV>(a.k_pages, kbase + (size_t)c * (kPage * 8), kc);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc = fmaf(qs[8 * c + e], kc[e], acc);
+      }
       if constexpr (KV == kFP8) acc *= a.kv_scales[2 * (size_t)page];
       z = acc * a.scale_log2;
     }
@@ -102,19 +133,26 @@ __global__ __launch_bounds__(64) void attn_generic_kernel(AttnArgs a) {
   sum = wave_sum(sum);
   __syncthreads();
 
-  // pass 2: lanes over head dims
+  // pass 2: lanes over head dims; V rows are dim-major ([D][16 tokens]), so
+  // four consecutive tokens of a row come in one load
   for (int d = lane; d < D; d += 64) {
     float acc = 0.f;
-    for (int t = 0; t < nkeys; ++t) {
-      const float p = ps[t];
-      if (p == 0.f) continue;
-      const int k = k0 + t / kPage;
-      const int tok = t % kPage;
+    for (int t0 = 0; t0 < nkeys; t0 += 4) {
+      const float p0 = ps[t0], p1 = ps[t0 + 1], p2 = ps[t0 + 2], p3 = ps[t0 + 3];
+      if (p0 == 0.f && p1 == 0.f && p2 == 0.f && p3 == 0.f) continue;
+      const int k = k0 + t0 / kPage;
+      const int tok = t0 % kPage;
       const int page = a.block_table[(size_t)b * a.bt_stride + k];
       const size_t vidx = (((size_t)page * a.Hkv + g) * D + d) * kPage + tok;
-      float v = load_elem<KV>(a.v_pages, vidx);
-      if constexpr (KV == kFP8) v *= a.kv_scales[2 * (size_t)page + 1];
-      acc = fmaf(p, v, acc);
+      float v[8];
+      load8<KV>(a.v_pages, vidx, v, true);
+      // a zero weight contributes nothing, whatever the slot holds (slots
+      // past the sequence end may hold anything, NaN included)
+      const float t_0 = p0 != 0.f ? p0 * v[0] : 0.f, t_1 = p1 != 0.f ? p1 * v[1] : 0.f;
+      const float t_2 = p2 != 0.f ? p2 * v[2] : 0.f, t_3 = p3 != 0.f ? p3 * v[3] : 0.f;
+      float s = (t_0 + t_1) + (t_2 + t_3);
+      if constexpr (KV == kFP8) s *= a.kv_scales[2 * (size_t)page + 1];
+      acc += s;
     }
     po[d] = acc / sum;
   }

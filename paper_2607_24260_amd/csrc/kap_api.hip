@@ -132,12 +132,30 @@ int blocks_per_cu(int id, int kv_type, int q_len) {
   return c > 0 ? c : 0;
 }
 
+// Generic path (one wavefront per query row and split): splits of at most
+// kGenericPagesPerSplit pages -- the keys one work item stages in LDS -- and,
+// when the call has few rows, more and smaller splits (down to
+// kGenericMinPagesPerSplit pages) until about kGenericTargetWaves wavefronts
+// run (the 4096-token fp32 workload: 32 rows x 2 splits of 36 pages took
+// 152 us per decode call). num_splits > 0 asks for at least that many.
+constexpr int kGenericTargetWaves = 4096;
+constexpr int kGenericMinPagesPerSplit = 4;
+int generic_splits(long long rows, int max_pages, int num_splits) {
+  const int lo = cdiv(max_pages, kap::kGenericPagesPerSplit);
+  const int hi = std::max(lo, cdiv(max_pages, kGenericMinPagesPerSplit));
+  long long want = rows > 0 ? (kGenericTargetWaves + rows - 1) / rows : 1;
+  if (num_splits > want) want = num_splits;
+  int n = (int)std::min<long long>(std::max<long long>(want, lo), hi);
+  if (num_splits > n) n = num_splits > max_pages ? max_pages : num_splits;
+  return n;
+}
+
 // Decode. Tuned path: with num_splits > 0, that many splits for every
 // (sequence, KV head); otherwise the balanced mode, where the kernel sizes
 // each sequence's splits from its view (about kDecodeTargetPerCU
 // workgroups per CU over the whole call) -- unless there are so many
 // (sequence, KV head) units that one split each already fills the device.
-// Generic path: splits of at most kGenericPagesPerSplit pages.
+// Generic path: see generic_splits.
 SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num_splits) {
   SplitPlan p{fast_geometry(kv), false, 1, 1, 0, 0, 0, 0};
   const int mb = max_blocks > 0 ? max_blocks : 1;
@@ -162,8 +180,7 @@ SplitPlan plan_decode(const kap_kv_cache *kv, int batch, int max_blocks, int num
     }
     p.pps = cdiv(mb, p.n_split);
   } else {
-    int n = cdiv(mb, kap::kGenericPagesPerSplit);
-    if (num_splits > n) n = num_splits > mb ? mb : num_splits;
+    const int n = generic_splits((long long)batch * kv->num_q_heads, mb, num_splits);
     p.pps = cdiv(mb, n);
     p.n_split = cdiv(mb, p.pps);
   }
@@ -200,8 +217,7 @@ SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_page
     }
     p.pps = 2 * cdiv(pairs, p.n_split);
   } else {
-    int n = cdiv(mp, kap::kGenericPagesPerSplit);
-    if (num_splits > n) n = num_splits > mp ? mp : num_splits;
+    const int n = generic_splits((long long)batch * q_len * kv->num_q_heads, mp, num_splits);
     p.pps = cdiv(mp, n);
     p.n_split = cdiv(mp, p.pps);
   }
