@@ -371,8 +371,10 @@ def _window(w, q_len, seed):
 @pytest.mark.parametrize("D,Hq,Hkv", [(64, 8, 4), (256, 16, 2), (128, 16, 8), (128, 32, 4)])
 @pytest.mark.parametrize("L,num_splits", [(900, 0), (3000, 0), (3000, 7)])
 def test_generic_path_geometries(kv_dtype, D, Hq, Hkv, L, num_splits):
-    # lengths L, L - 1 and 37 (partial last pages); 900 tokens fit one generic
-    # split (<= 64 pages), 3000 take three, num_splits = 7 forces seven
+    # lengths L, L - 1 and 37 (partial last pages); with this few query rows
+    # the generic path splits the keys into pieces of 4 pages and more (9-15
+    # splits at 900 tokens, 9-47 at 3000, by call); num_splits = 7 asks for
+    # at least seven
     cfg = 2 if kv_dtype == "bf16" else 5
     # (the ragged fp8 recipe draws its lengths from [4096, seq_len])
     w, pool = _ragged(cfg, 3, max(L, 1000) if cfg == 2 else 5000, [L, L - 1, 37],
