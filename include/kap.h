@@ -225,7 +225,11 @@ kap_status kap_compile_plan_masked(int32_t batch, const int32_t *seq_lens,
  * num_splits (host): 0 = automatic -- the tuned path then sizes the key
  * splits of each (sequence, KV head) on the device from that sequence's
  * actual view, so ragged batches stay balanced; n > 0 forces n key splits
- * per (sequence, KV head) (clamped to max_view_blocks).
+ * per (sequence, KV head) on the tuned path (clamped to max_view_blocks).
+ * The generic path (other geometries and dtypes) splits keys into pieces of
+ * at most 64 pages, finer when the call has few query rows, and takes at
+ * least n pieces when n > 0. Results do not depend on the split count
+ * beyond rounding.
  * Passing the full block table as the view, with view_logical_block[b][j] = j
  * and view_num_blocks[b] = ceil(seq_lens[b]/16), is full-context decode.
  */
