@@ -2,10 +2,11 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
 
-A step is one pass of the whole hot path over one batch: kap_compile_plan, then
-the proposal / verify schedule of the workload (for the 128K workload: 64
-selected-view decode calls and 16 verify calls with a gamma = 4 window,
-interleaved 4 : 1). Every call reads the KV pool of its own "layer replica";
+A step is one pass of the whole hot path over one batch: kap_compile_plan,
+kap_decode_schedule (the decode calls' split assignment for the plan's view,
+written once), then the proposal / verify schedule of the workload (for the 128K
+workload: 64 selected-view decode calls and 16 verify calls with a gamma = 4
+window, interleaved 4 : 1). Every call reads the KV pool of its own "layer replica";
 the replicas rotate so that the bytes touched between two reads of the same
 buffer far exceed the 256 MB Infinity Cache -- the numbers are HBM numbers.
 
@@ -267,11 +268,15 @@ def _attention_calls(torch, K, w, R, dev):
                        dtype=torch.uint8, device=dev)
     ws_v = torch.zeros(max(256, K.verify_workspace_bytes(kvs[0], B, q_len, Lmax)),
                        dtype=torch.uint8, device=dev)
+    sv = K.decode_schedule(kvs[0], seq_lens, plan["view_block_table"],
+                           plan["view_logical_block"], plan["view_num_blocks"], cap)
+    sf = K.decode_schedule(kvs[0], seq_lens, fbt, lblk_f, nb_f, fbt.shape[1])
     view = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens, plan["view_block_table"],
                                    plan["view_logical_block"], plan["view_num_blocks"], cap,
-                                   w.sm_scale, o, l, ws_d) for r in range(R)]
+                                   w.sm_scale, o, l, ws_d, schedule=sv) for r in range(R)]
     full = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens, fbt, lblk_f, nb_f,
-                                   fbt.shape[1], w.sm_scale, o, l, ws_d) for r in range(R)]
+                                   fbt.shape[1], w.sm_scale, o, l, ws_d, schedule=sf)
+            for r in range(R)]
     ver = [K.bind_verify(kvs[r], w.q_verify[0], seq_lens, fbt, Lmax, w.sm_scale, ov, lv, ws_v)
            for r in range(R)]
     t_view = time_loop(lambda i: view[i % R](), max(64, 3 * R), 5, torch)
@@ -327,9 +332,12 @@ def config_figures(torch, K, dev, cfg, with_cpu):
         l = torch.empty((B, Hq), dtype=torch.float32, device=dev)
         ws = torch.zeros(max(256, K.selected_decode_workspace_bytes(kvs[0], B, cap)),
                          dtype=torch.uint8, device=dev)
+        sch = K.decode_schedule(kvs[0], seq_lens, plan["view_block_table"],
+                                plan["view_logical_block"], plan["view_num_blocks"], cap)
         calls = [[K.bind_selected_decode(kvs[r], w.q_decode[s], seq_lens,
                                          plan["view_block_table"], plan["view_logical_block"],
-                                         plan["view_num_blocks"], cap, w.sm_scale, o, l, ws)
+                                         plan["view_num_blocks"], cap, w.sm_scale, o, l, ws,
+                                         schedule=sch)
                   for s in range(nq)] for r in range(R)]
         t = time_loop(lambda i: calls[i % R][i % nq](), max(200, 3 * R), 5, torch)
         nbytes = algorithmic_bytes(w, vt, vb, "decode")
@@ -704,16 +712,22 @@ def main():
              torch.empty((B, q_len, Hq, D), dtype=torch.float32, device=dev),
              torch.empty((B, q_len, Hq), dtype=torch.float32, device=dev)) for _ in range(R)]
 
+    # the decode calls' split assignment, written once per plan (kap_decode_schedule)
+    view_args = (seq_lens, plan_out["view_block_table"], plan_out["view_logical_block"],
+                 plan_out["view_num_blocks"], cap)
+    dsched = K.decode_schedule(kvs[0], *view_args)
+    sched_call = K.bind_decode_schedule(kvs[0], *view_args, dsched)
+
+    def bind_decodes(stream, schedule):
+        return [[K.bind_selected_decode(kvs[r], w.q_decode[s], *view_args, w.sm_scale,
+                                        outs[r][0], outs[r][1], ws_dec, schedule=schedule,
+                                        stream=stream)
+                 for s in range(w.q_decode.shape[0])] for r in range(R)]
+
     def bind_calls(stream):
-        dcs, vcs = [], []
+        dcs, vcs = bind_decodes(stream, dsched), []
         for r in range(R):
             o, l, ov, lv = outs[r]
-            dcs.append([K.bind_selected_decode(kvs[r], w.q_decode[s], seq_lens,
-                                               plan_out["view_block_table"],
-                                               plan_out["view_logical_block"],
-                                               plan_out["view_num_blocks"], cap, w.sm_scale,
-                                               o, l, ws_dec, stream=stream)
-                        for s in range(w.q_decode.shape[0])])
             vcs.append([K.bind_verify(kvs[r], w.q_verify[j], seq_lens, fbt,
                                       int(w.seq_lens.max()), w.sm_scale, ov, lv, ws_ver,
                                       stream=stream)
@@ -726,8 +740,9 @@ def main():
     n_dec = sum(1 for k, _ in sched if k == "decode")
     n_ver = len(sched) - n_dec
 
-    def step_with(pc, dcs, vcs):
+    def step_with(pc, sc, dcs, vcs):
         pc()
+        sc()
         for c, (kind, i) in enumerate(sched):
             r = c % R
             if kind == "decode":
@@ -736,7 +751,7 @@ def main():
                 vcs[r][i]()
 
     def step(_):
-        step_with(plan_call, dec_calls, ver_calls)
+        step_with(plan_call, sched_call, dec_calls, ver_calls)
 
     dec_b = algorithmic_bytes(w, view_tokens, view_blocks, "decode")
     ver_b = algorithmic_bytes(w, view_tokens, view_blocks, "verify", q_len)
@@ -773,11 +788,12 @@ def main():
     with torch.cuda.stream(gs):
         g_plan = K.bind_compile_plan(*plan_in, num_pages=w.num_pages, view_capacity=cap,
                                      out=plan_out, workspace=ws_plan, stream=gs)
+        g_sched = K.bind_decode_schedule(kvs[0], *view_args, dsched, stream=gs)
         g_dec, g_ver = bind_calls(gs)
     gs.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=gs):
-        step_with(g_plan, g_dec, g_ver)
+        step_with(g_plan, g_sched, g_dec, g_ver)
     with torch.cuda.stream(gs):
         for _ in range(max(args.warmup, 1)):
             graph.replay()
@@ -789,12 +805,15 @@ def main():
         ge_ev.record(gs)
     torch.cuda.synchronize()
     ms_step_graph = gs_ev.elapsed_time(ge_ev) / args.steps
-    log(f"step as one HIP graph: {ms_step_graph:.3f} ms ({len(sched) + 1} launches per step)")
+    log(f"step as one HIP graph: {ms_step_graph:.3f} ms ({len(sched) + 2} launches per step)")
     del graph
 
     # per-call rates, rotating replicas (HBM) and on one buffer (cache-hot, context)
     nq = w.q_decode.shape[0]
     t_dec = time_loop(lambda i: dec_calls[i % R][i % nq](), 256, 5, torch)
+    dec_bal = bind_decodes(None, None)      # the same calls computing the split map themselves
+    t_dec_bal = time_loop(lambda i: dec_bal[i % R][i % nq](), 256, 5, torch)
+    t_sched = time_loop(lambda i: sched_call(), 50, 3, torch)
     t_dec_hot = time_loop(lambda i: dec_calls[0][i % nq](), 256, 5, torch)
     t_ver = time_loop(lambda i: ver_calls[i % R][i % len(w.q_verify)](), 48, 3, torch)
     t_plan = time_loop(lambda i: plan_call(), 50, 3, torch)
@@ -824,9 +843,11 @@ def main():
         l_c = torch.empty((B, Hq), dtype=torch.float32, device=dev)
         ws_c = torch.zeros(max(256, K.selected_decode_workspace_bytes(comp[0], B, cap_c)),
                            dtype=torch.uint8, device=dev)
+        s_c = K.decode_schedule(comp[0], seq_lens, ctab, lblk_c, plan_out["view_num_blocks"],
+                                cap_c)
         dec_c = [K.bind_selected_decode(comp[c], w.q_decode[0], seq_lens, ctab, lblk_c,
                                         plan_out["view_num_blocks"], cap_c, w.sm_scale, o_c, l_c,
-                                        ws_c) for c in range(R)]
+                                        ws_c, schedule=s_c) for c in range(R)]
         t_dec_c = time_loop(lambda i: dec_c[i % R](), 256, 5, torch)
         win = q_len * B
         Lh = np.asarray(w.seq_lens, dtype=np.int64)
@@ -860,8 +881,9 @@ def main():
                            dtype=torch.uint8, device=dev)
         o_f = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
         l_f = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        s_f = K.decode_schedule(kvs[0], seq_lens, fbt, lblk_f, nb_f, fbt.shape[1])
         dec_f = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens, fbt, lblk_f, nb_f,
-                                        fbt.shape[1], w.sm_scale, o_f, l_f, ws_f)
+                                        fbt.shape[1], w.sm_scale, o_f, l_f, ws_f, schedule=s_f)
                  for r in range(R)]
         t_full = time_loop(lambda i: dec_f[i % R](), 27, 3, torch)
         rep_ = costmodel.measured(q_len - 1, costmodel.expected_acceptance(q_len - 1),
@@ -898,11 +920,15 @@ def main():
         vb_tok = plan_tok["view_num_blocks"].cpu().numpy()
         o_t = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
         l_t = torch.empty((B, Hq), dtype=torch.float32, device=dev)
+        s_t = K.decode_schedule(kvs[0], seq_lens, plan_tok["view_block_table"],
+                                plan_tok["view_logical_block"], plan_tok["view_num_blocks"], cap,
+                                view_token_mask=plan_tok["view_token_mask"])
         dec_t = [K.bind_selected_decode(kvs[r], w.q_decode[0], seq_lens,
                                         plan_tok["view_block_table"],
                                         plan_tok["view_logical_block"],
                                         plan_tok["view_num_blocks"], cap, w.sm_scale, o_t, l_t,
-                                        ws_dec, view_token_mask=plan_tok["view_token_mask"])
+                                        ws_dec, view_token_mask=plan_tok["view_token_mask"],
+                                        schedule=s_t)
                  for r in range(R)]
         t_dec_t = time_loop(lambda i: dec_t[i % R](), 256, 5, torch)
         t_plan_t = time_loop(lambda i: plan_tok_call(), 50, 3, torch)
@@ -995,6 +1021,8 @@ def main():
         "decode_effective_gbs": round(dec_gbs, 1),
         "decode_pct_hbm_peak": round(100 * dec_gbs / HBM_PEAK_GBS, 2),
         "decode_cache_hot_us_per_call": round(t_dec_hot * 1e3, 3),
+        "decode_unscheduled_us_per_call": round(t_dec_bal * 1e3, 3),
+        "decode_schedule_us_per_call": round(t_sched * 1e3, 2),
         "verify_calls_per_s": round(1e3 / t_ver, 1),
         "verify_us_per_call": round(t_ver * 1e3, 2),
         "verify_effective_gbs": round(ver_gbs, 1),

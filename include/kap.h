@@ -289,6 +289,57 @@ kap_status kap_selected_decode_noalloc(const kap_kv_cache *kv, int32_t batch, co
                                        void *stream);
 
 /*
+ * kap_decode_schedule / kap_selected_decode_scheduled -- kap_selected_decode
+ * with its split assignment computed once per view. The view stays fixed over
+ * the k proposal steps of a cycle (Sec. 3.2, "Selected-KV proposal"), so the
+ * balanced split map that kap_selected_decode derives at the start of every
+ * call from all view lengths -- before its first page loads -- can be derived
+ * once by kap_decode_schedule and reused by every decode call on that view:
+ * each workgroup then starts from its record (its work item and its
+ * wavefronts' first view entries) and issues its first page loads at once.
+ *
+ * kap_decode_schedule_bytes returns the schedule size for the kv geometry,
+ * batch and max_view_blocks on the current device; 0 means these calls use
+ * no balanced map (one split per (sequence, KV head), or the generic path),
+ * and the schedule is then neither written nor read (it may be NULL).
+ * kap_decode_schedule writes the schedule -- caller-owned device memory,
+ * 16-byte aligned -- from seq_lens, the view arrays (view_token_mask NULL for
+ * page-granular views) and view_num_blocks, laid out as for
+ * kap_selected_decode.
+ *
+ * kap_selected_decode_scheduled takes the arguments of kap_selected_decode
+ * with num_splits = 0 (view_token_mask NULL: page-granular; otherwise as
+ * kap_selected_decode_masked) plus the schedule, and returns the same results
+ * bit for bit. The schedule must have been written by kap_decode_schedule on
+ * this device for the same kv geometry and dtypes, batch, seq_lens, view
+ * arrays, view_stride, view_num_blocks and max_view_blocks, unchanged since
+ * (write it again whenever kap_compile_plan or kap_fallback_update rewrites
+ * the view). With any other schedule the results, and the workspace's
+ * arrival counters, are undefined; no memory outside the arrays passed is
+ * accessed even then. Errors: those of kap_selected_decode; a NULL schedule
+ * where kap_decode_schedule_bytes is non-zero is KAP_ERR_INVALID_ARGUMENT.
+ */
+size_t kap_decode_schedule_bytes(const kap_kv_cache *kv, int32_t batch,
+                                 int32_t max_view_blocks);
+
+kap_status kap_decode_schedule(const kap_kv_cache *kv, int32_t batch, const int32_t *seq_lens,
+                               const int32_t *view_block_table,
+                               const int32_t *view_logical_block,
+                               const uint32_t *view_token_mask, int32_t view_stride,
+                               const int32_t *view_num_blocks, int32_t max_view_blocks,
+                               int32_t *schedule, size_t schedule_bytes, void *stream);
+
+kap_status kap_selected_decode_scheduled(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                         const int32_t *seq_lens,
+                                         const int32_t *view_block_table,
+                                         const int32_t *view_logical_block,
+                                         const uint32_t *view_token_mask, int32_t view_stride,
+                                         const int32_t *view_num_blocks, int32_t max_view_blocks,
+                                         const int32_t *schedule, float sm_scale, float *out,
+                                         float *lse, void *workspace, size_t workspace_bytes,
+                                         void *stream);
+
+/*
  * kap_verify -- full-context verification attention of the q_len = k+1
  * window (Sec. 3.2, "Full-context verification"; Eq. (2)).
  *

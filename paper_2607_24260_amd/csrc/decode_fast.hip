@@ -170,8 +170,15 @@ __device__ __forceinline__ void mask_v(PageRegs<KV> &r, uint32_t vis) {
   }
 }
 
-template <int KV, int RING, bool BALANCED, bool MASKED>
+// How a workgroup finds its work item: uniform splits (the grid is
+// (n_split, Hkv, batch)), the balanced map computed here, or the balanced
+// map's record precomputed for the view by decode_schedule_kernel.
+enum DecodeMode { kUniform, kBalanced, kScheduled };
+
+template <int KV, int RING, int MODE, bool MASKED>
 __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
+  constexpr bool BALANCED = MODE == kBalanced;
+  static_assert(MODE != kScheduled || RING == 2, "schedule records hold two ring entries");
   __shared__ __attribute__((aligned(16))) uint16_t pw_hi[kWaves][4][kPage];   // weights (x V scale), bf16 hi + lo
   __shared__ __attribute__((aligned(16))) uint16_t pw_lo[kWaves][4][kPage];
   __shared__ float wstat[2][kWaves][4];            // per-wave m (log2) and l per head
@@ -191,7 +198,8 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
   // computed -- the even assignment, a.guess_splits splits per unit, which
   // the map produces for equal views -- and read again if the map differs.
   WorkItem wi;
-  if constexpr (BALANCED) {
+  if constexpr (MODE == kScheduled) {
+  } else if constexpr (BALANCED) {
     const int ng = a.guess_splits;
     const int w = blockIdx.x;
     const int q = div_u21(w, ng);   // w < slots < 2^21
@@ -230,7 +238,28 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     }
   };
   int L, nb;
-  if constexpr (BALANCED) {
+  if constexpr (MODE == kScheduled) {
+    // the record of this workgroup (uniform address: scalar loads), clamped
+    // so that a record that does not belong to these arguments cannot lead
+    // outside the arrays
+    const int32_t *rec = a.schedule + (size_t)blockIdx.x * kSchedInts;
+    wi.n_split = rec[kSchedNSplit];
+    if (wi.n_split <= 0) return;
+    wi.n_split = min(wi.n_split, a.n_split);
+    wi.b = min(max(rec[kSchedB], 0), a.batch - 1);
+    wi.g = min(max(rec[kSchedG], 0), a.Hkv - 1);
+    wi.split = min(max(rec[kSchedSplit], 0), wi.n_split - 1);
+    wi.slot0 = min(max(rec[kSchedSlot0], 0), a.n_split - wi.n_split);
+    L = rec[kSchedL];
+    nb = min(max(rec[kSchedNb], 0), a.max_blocks);
+#pragma unroll
+    for (int j = 0; j < RING; ++j) {
+      const int32_t *e = rec + kSchedEntries + 3 * (2 * wave + j);
+      raw_pg[j] = e[0];
+      raw_lb[j] = e[1];
+      raw_mk[j] = MASKED ? (uint32_t)e[2] : 0xFFFFu;
+    }
+  } else if constexpr (BALANCED) {
     // view pages of sequence bb (per KV head) decide its split count
     auto load = [&](int bb) {
       return SeqLoad{max(0, min(a.num_blocks[bb], a.max_blocks)), a.seq_lens[bb]};
@@ -491,12 +520,53 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
 
 template <int KV, int RING, bool MASKED>
 void launch_mode(const AttnArgs &a, hipStream_t s) {
-  if (a.ragged)
-    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, true, MASKED>), dim3(a.n_split), dim3(256),
-                       0, s, a);
+  if (a.ragged && a.schedule)
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, kScheduled, MASKED>), dim3(a.n_split),
+                       dim3(256), 0, s, a);
+  else if (a.ragged)
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, kBalanced, MASKED>), dim3(a.n_split),
+                       dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, false, MASKED>),
+    hipLaunchKernelGGL((decode_fast_kernel<KV, RING, kUniform, MASKED>),
                        dim3(a.n_split, a.Hkv, a.batch), dim3(256), 0, s, a);
+}
+
+// One wavefront per balanced-mode workgroup w: the map's work item for w and
+// the first two view entries of each of its four wavefronts, as a record.
+// Workgroups past the last slot get a record with no work.
+__global__ __launch_bounds__(64) void decode_schedule_kernel(AttnArgs a) {
+  const int lane = threadIdx.x;
+  auto load = [&](int bb) {
+    return SeqLoad{max(0, min(a.num_blocks[bb], a.max_blocks)), a.seq_lens[bb]};
+  };
+  const SeqLoad first = map_first_loads(a, load);
+  WorkItem wi;
+  int nb = 0, L = 0;
+  const bool live = ragged_map(a, load, first, blockIdx.x, wi, nb, L);
+  int32_t *rec = a.schedule_out + (size_t)blockIdx.x * kSchedInts;
+  if (!live) {
+    if (lane < kSchedEntries) rec[lane] = 0;
+    return;
+  }
+  if (lane < kSchedEntries) {
+    const int v[kSchedEntries] = {wi.b, wi.g, wi.split, wi.n_split, wi.slot0, L, nb, 0};
+    int x = 0;
+#pragma unroll
+    for (int f = 0; f < kSchedEntries; ++f) x = lane == f ? v[f] : x;
+    rec[lane] = x;
+  }
+  if (lane < 2 * kWaves) {
+    // lane 2 w + j: ring slot j of wavefront w, view entry
+    // (4 split + w) + 4 n_split j of the sequence (clamped to the row)
+    const int w = lane >> 1, j = lane & 1;
+    const int last_entry = max(a.max_blocks - 1, 0);
+    const int kk = min(wi.split * kWaves + w + wi.n_split * kWaves * j, last_entry);
+    const size_t at = (size_t)wi.b * a.bt_stride + kk;
+    int32_t *e = rec + kSchedEntries + 3 * lane;
+    e[0] = a.block_table[at];
+    e[1] = a.logical_block[at];
+    e[2] = a.token_mask ? (int32_t)a.token_mask[at] : 0xFFFF;
+  }
 }
 
 template <int KV, int RING>
@@ -510,6 +580,11 @@ hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
 
 }  // namespace
 
+hipError_t launch_decode_schedule(const AttnArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(decode_schedule_kernel, dim3(a.n_split), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s) {
   if (a.kv_type == kBF16) return launch_kv<kBF16, kRingBF16>(a, s);
   if (a.kv_type == kFP8) return launch_kv<kFP8, kRingFP8>(a, s);
@@ -521,9 +596,9 @@ int decode_fast_blocks_per_cu(int kv_type) {
   const hipError_t e =
       kv_type == kFP8
           ? hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &nb, decode_fast_kernel<kFP8, kRingFP8, true, false>, 256, 0)
+                &nb, decode_fast_kernel<kFP8, kRingFP8, kBalanced, false>, 256, 0)
           : hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &nb, decode_fast_kernel<kBF16, kRingBF16, true, false>, 256, 0);
+                &nb, decode_fast_kernel<kBF16, kRingBF16, kBalanced, false>, 256, 0);
   return e == hipSuccess ? nb : 0;
 }
 

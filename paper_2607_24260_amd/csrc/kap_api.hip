@@ -492,7 +492,8 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
                                   int32_t view_stride, const int32_t *view_num_blocks,
                                   int32_t max_view_blocks, float sm_scale, int32_t num_splits,
                                   float *out, float *lse, void *workspace,
-                                  size_t workspace_bytes, void *stream, bool noalloc = false) {
+                                  size_t workspace_bytes, void *stream, bool noalloc = false,
+                                  const int32_t *schedule = nullptr, bool scheduled = false) {
   kap_status st = check_kv(kv);
   if (st != KAP_OK) return st;
   if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
@@ -515,6 +516,10 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
   if (!aligned(q, 16) || !aligned(out, 16))
     return fail(KAP_ERR_INVALID_ARGUMENT, "q and out must be 16-byte aligned");
   const SplitPlan p = plan_decode(kv, batch, max_view_blocks, num_splits);
+  if (scheduled && p.fast && p.ragged && !schedule)
+    return fail(KAP_ERR_INVALID_ARGUMENT,
+                "schedule is NULL (kap_decode_schedule_bytes is %zu for these arguments)",
+                (size_t)p.n_split * kap::kSchedInts * sizeof(int32_t));
   WsLayout layout = ws_layout(kv, batch, 1, p);
   if (noalloc) {
     // the library's own scratch instead of a workspace
@@ -574,6 +579,7 @@ static kap_status selected_decode(const kap_kv_cache *kv, int32_t batch, const v
   a.scale_log2 = sm_scale * kap::kLog2e;
   a.out = out;
   a.lse = lse;
+  a.schedule = scheduled && p.fast && p.ragged ? schedule : nullptr;
   return launch_attention(a, kv, p, true, workspace, layout, static_cast<hipStream_t>(stream));
 }
 
@@ -598,6 +604,84 @@ kap_status kap_selected_decode_masked(const kap_kv_cache *kv, int32_t batch, con
   return selected_decode(kv, batch, q, seq_lens, view_block_table, view_logical_block,
                          view_token_mask, true, view_stride, view_num_blocks, max_view_blocks,
                          sm_scale, num_splits, out, lse, workspace, workspace_bytes, stream);
+}
+
+size_t kap_decode_schedule_bytes(const kap_kv_cache *kv, int32_t batch,
+                                 int32_t max_view_blocks) {
+  if (check_kv(kv) != KAP_OK || batch <= 0 || max_view_blocks < 0) return 0;
+  const SplitPlan p = plan_decode(kv, batch, max_view_blocks, 0);
+  return p.fast && p.ragged ? (size_t)p.n_split * kap::kSchedInts * sizeof(int32_t) : 0;
+}
+
+kap_status kap_decode_schedule(const kap_kv_cache *kv, int32_t batch, const int32_t *seq_lens,
+                               const int32_t *view_block_table,
+                               const int32_t *view_logical_block,
+                               const uint32_t *view_token_mask, int32_t view_stride,
+                               const int32_t *view_num_blocks, int32_t max_view_blocks,
+                               int32_t *schedule, size_t schedule_bytes, void *stream) {
+  kap_status st = check_kv(kv);
+  if (st != KAP_OK) return st;
+  if (batch < 0) return fail(KAP_ERR_INVALID_ARGUMENT, "batch < 0");
+  if (batch > 65535) return fail(KAP_ERR_UNSUPPORTED, "batch %d > 65535", batch);
+  if (max_view_blocks < 0 || view_stride < max_view_blocks)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "need 0 <= max_view_blocks (%d) <= view_stride (%d)",
+                max_view_blocks, view_stride);
+  const size_t need = kap_decode_schedule_bytes(kv, batch, max_view_blocks);
+  if (need == 0) return ok();   // no balanced split map for these arguments: nothing to record
+  if (!seq_lens || !view_num_blocks)
+    return fail(KAP_ERR_INVALID_ARGUMENT, "a required pointer is NULL");
+  if (max_view_blocks > 0 && (!view_block_table || !view_logical_block))
+    return fail(KAP_ERR_INVALID_ARGUMENT, "view tables are NULL");
+  if (!schedule || schedule_bytes < need)
+    return fail(KAP_ERR_WORKSPACE_TOO_SMALL, "schedule needs %zu bytes, got %zu", need,
+                schedule_bytes);
+  if (!aligned(schedule, 16)) return fail(KAP_ERR_INVALID_ARGUMENT, "schedule must be 16-byte aligned");
+  const SplitPlan p = plan_decode(kv, batch, max_view_blocks, 0);
+  kap::AttnArgs a;
+  a.batch = batch;
+  a.Hq = kv->num_q_heads;
+  a.Hkv = kv->num_kv_heads;
+  a.G = kv->num_q_heads / kv->num_kv_heads;
+  a.D = kv->head_dim;
+  a.kv_type = kv->kv_dtype;
+  a.num_pages = kv->num_pages;
+  a.q_len = 1;
+  a.seq_lens = seq_lens;
+  const bool no_table = max_view_blocks == 0;
+  a.block_table = no_table ? seq_lens : view_block_table;
+  a.bt_stride = no_table ? 0 : view_stride;
+  a.logical_block = no_table ? seq_lens : view_logical_block;
+  a.token_mask = view_token_mask && !no_table ? view_token_mask : nullptr;
+  a.num_blocks = view_num_blocks;
+  a.max_blocks = max_view_blocks;
+  a.n_split = p.n_split;
+  a.ragged = 1;
+  a.w_target = p.w_target;
+  a.w_uneven = p.w_uneven;
+  a.min_chunk = p.min_chunk;
+  a.rcp_w_target = p.w_target > 0 ? 1.0 / p.w_target : 0.0;
+  a.rcp_w_uneven = p.w_uneven > 0 ? 1.0 / p.w_uneven : 0.0;
+  a.schedule_out = schedule;
+  (void)hipGetLastError();
+  const hipError_t e = kap::launch_decode_schedule(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess)
+    return fail(KAP_ERR_HIP, "decode_schedule launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+kap_status kap_selected_decode_scheduled(const kap_kv_cache *kv, int32_t batch, const void *q,
+                                         const int32_t *seq_lens,
+                                         const int32_t *view_block_table,
+                                         const int32_t *view_logical_block,
+                                         const uint32_t *view_token_mask, int32_t view_stride,
+                                         const int32_t *view_num_blocks, int32_t max_view_blocks,
+                                         const int32_t *schedule, float sm_scale, float *out,
+                                         float *lse, void *workspace, size_t workspace_bytes,
+                                         void *stream) {
+  return selected_decode(kv, batch, q, seq_lens, view_block_table, view_logical_block,
+                         view_token_mask, view_token_mask != nullptr, view_stride,
+                         view_num_blocks, max_view_blocks, sm_scale, 0, out, lse, workspace,
+                         workspace_bytes, stream, false, schedule, true);
 }
 
 kap_status kap_selected_decode_noalloc(const kap_kv_cache *kv, int32_t batch, const void *q,

@@ -94,9 +94,22 @@ struct AttnArgs {
   // decode over a token-granular view: [batch][bt_stride] masks, bit t = token
   // t of the view page is visible; NULL: every token below seq_len is
   const uint32_t *token_mask = nullptr;
+  // decode, balanced mode with a precomputed schedule (kap_decode_schedule):
+  // one kSchedInts record per workgroup; NULL: the kernel computes the map
+  const int32_t *schedule = nullptr;
+  int32_t *schedule_out = nullptr;   // kap_decode_schedule: the records written
   float *out;       // [batch * R][D]
   float *lse;       // [batch * R]
 };
+
+// Decode schedule record of workgroup w (int32 fields): the work item the
+// balanced map gives w -- sequence, KV head, split, split count (0: no work),
+// first slot -- the sequence's length and view blocks, and the first two view
+// entries of each of the four wavefronts (page id, logical block, token mask)
+// that start its page ring.
+constexpr int kSchedInts = 32;
+enum SchedField { kSchedB, kSchedG, kSchedSplit, kSchedNSplit, kSchedSlot0, kSchedL, kSchedNb,
+                  kSchedEntries = 8 };   // + 3 * (2 * wave + ring slot) + {page, lblk, mask}
 
 // kap_append_kv after host validation.
 struct AppendArgs {
@@ -155,6 +168,7 @@ hipError_t launch_append_kv(const AppendArgs &a, hipStream_t s);
 hipError_t launch_compact_view(const CompactArgs &a, int grid, hipStream_t s);
 hipError_t launch_attn_generic(const AttnArgs &a, hipStream_t s);
 hipError_t launch_decode_fast(const AttnArgs &a, hipStream_t s);
+hipError_t launch_decode_schedule(const AttnArgs &a, hipStream_t s);
 hipError_t launch_verify_mfma(const AttnArgs &a, hipStream_t s);
 hipError_t launch_merge(const AttnArgs &a, hipStream_t s);
 hipError_t launch_stream_read(const void *src, size_t bytes, uint32_t *sink, hipStream_t s);

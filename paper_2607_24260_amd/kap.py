@@ -46,7 +46,8 @@ PAGE = 16
 EXPORTS = (
     "kap_compile_plan", "kap_compile_plan_workspace_bytes", "kap_compile_plan_masked",
     "kap_selected_decode", "kap_selected_decode_workspace_bytes", "kap_selected_decode_masked",
-    "kap_selected_decode_noalloc",
+    "kap_selected_decode_noalloc", "kap_decode_schedule_bytes", "kap_decode_schedule",
+    "kap_selected_decode_scheduled",
     "kap_verify", "kap_verify_workspace_bytes",
     "kap_append_kv", "kap_compact_view", "kap_fallback_update", "kap_fallback_update_masked",
     "kap_accept_top3", "kap_accept_top3_workspace_bytes",
@@ -115,6 +116,15 @@ def load_library(path: str = LIB_PATH):
     lib.kap_selected_decode_noalloc.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _I32, _P, _I32, _F, _I32,
         _P, _P, _P]
+    lib.kap_decode_schedule_bytes.restype = _SZ
+    lib.kap_decode_schedule_bytes.argtypes = [ctypes.POINTER(KVCacheStruct), _I32, _I32]
+    lib.kap_decode_schedule.restype = _I32
+    lib.kap_decode_schedule.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _I32, _P, _I32, _P, _SZ, _P]
+    lib.kap_selected_decode_scheduled.restype = _I32
+    lib.kap_selected_decode_scheduled.argtypes = [
+        ctypes.POINTER(KVCacheStruct), _I32, _P, _P, _P, _P, _P, _I32, _P, _I32, _P, _F,
+        _P, _P, _P, _SZ, _P]
     lib.kap_selected_decode_workspace_bytes.restype = _SZ
     lib.kap_selected_decode_workspace_bytes.argtypes = [
         ctypes.POINTER(KVCacheStruct), _I32, _I32, _I32]
@@ -519,8 +529,9 @@ def _outputs(shape, dev, out, lse):
 
 def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
                  view_num_blocks, max_view_blocks, sm_scale, num_splits, out, lse, workspace,
-                 view_token_mask, stream, noalloc=False):
-    """Validate and marshal one kap_selected_decode[_masked] call."""
+                 view_token_mask, stream, noalloc=False, schedule=None):
+    """Validate and marshal one kap_selected_decode[_masked] call, or with
+    ``schedule`` (from decode_schedule) a kap_selected_decode_scheduled one."""
     lib = load_library()
     _dev(q, "q", kv.q_dtype, 3)
     B = q.shape[0]
@@ -538,6 +549,14 @@ def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
             raise ValueError("view_token_mask must be shaped like the view tables")
     if seq_lens.shape[0] != B or view_num_blocks.shape[0] != B:
         raise ValueError("seq_lens / view_num_blocks must have batch entries")
+    if schedule is not None:
+        if num_splits != 0:
+            raise ValueError("a scheduled decode takes num_splits = 0")
+        nbytes = decode_schedule_bytes(kv, B, max_view_blocks)
+        if nbytes:
+            _dev(schedule, "schedule", torch.int32, 1)
+        if schedule.numel() * 4 < nbytes:
+            raise ValueError(f"schedule of {nbytes} bytes required")
     need = 0 if noalloc else selected_decode_workspace_bytes(kv, B, max_view_blocks, num_splits)
     with torch.cuda.stream(stream):
         out, lse = _outputs((B, kv.num_q_heads, kv.head_dim), q.device, out, lse)
@@ -548,25 +567,95 @@ def _decode_call(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
     tail = (view_block_table.shape[1], _ptr(view_num_blocks), int(max_view_blocks),
             float(sm_scale), int(num_splits), _ptr(out), _ptr(lse), _ptr(workspace), have,
             _stream(stream))
-    fn = lib.kap_selected_decode if view_token_mask is None else lib.kap_selected_decode_masked
     keep = (kv, q, seq_lens, view_block_table, view_logical_block, view_num_blocks,
-            view_token_mask, out, lse, workspace)
+            view_token_mask, out, lse, workspace, schedule)
+    if schedule is not None:
+        args = head + (_ptr(view_token_mask), view_block_table.shape[1], _ptr(view_num_blocks),
+                       int(max_view_blocks),
+                       _ptr(schedule) if schedule.numel() else None, float(sm_scale),
+                       _ptr(out), _ptr(lse), _ptr(workspace), have, _stream(stream))
+        return lib.kap_selected_decode_scheduled, args, (out, lse), keep
+    fn = lib.kap_selected_decode if view_token_mask is None else lib.kap_selected_decode_masked
     return fn, head + mask + tail, (out, lse), keep
 
 
 def selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
                     view_num_blocks, max_view_blocks: int, sm_scale: float, *,
                     num_splits: int = 0, out=None, lse=None, workspace=None,
-                    view_token_mask=None, stream=None):
+                    view_token_mask=None, schedule=None, stream=None):
     """One proposal step over the selected-KV view. q [B][Hq][D]; returns
     (out [B][Hq][D] float32, lse [B][Hq] float32). ``view_token_mask``
     [B][view_stride] (a token-granular plan's masks) calls
-    kap_selected_decode_masked."""
+    kap_selected_decode_masked; ``schedule`` (decode_schedule's output for
+    this view) calls kap_selected_decode_scheduled."""
     fn, args, res, _ = _decode_call(kv, q, seq_lens, view_block_table, view_logical_block,
                                     view_num_blocks, max_view_blocks, sm_scale, num_splits,
-                                    out, lse, workspace, view_token_mask, stream)
+                                    out, lse, workspace, view_token_mask, stream,
+                                    schedule=schedule)
     _check(fn(*args))
     return res
+
+
+def decode_schedule_bytes(kv: KVCache, batch: int, max_view_blocks: int) -> int:
+    return int(load_library().kap_decode_schedule_bytes(ctypes.byref(kv.struct), int(batch),
+                                                        int(max_view_blocks)))
+
+
+def _schedule_call(kv: KVCache, seq_lens, view_block_table, view_logical_block,
+                   view_num_blocks, max_view_blocks, view_token_mask, out, stream):
+    """Validate and marshal one kap_decode_schedule call: (args, out)."""
+    _dev(seq_lens, "seq_lens", torch.int32, 1)
+    _dev(view_num_blocks, "view_num_blocks", torch.int32, 1)
+    _dev(view_block_table, "view_block_table", torch.int32, 2)
+    _dev(view_logical_block, "view_logical_block", torch.int32, 2)
+    B = seq_lens.shape[0]
+    if view_block_table.shape != view_logical_block.shape or view_block_table.shape[0] != B:
+        raise ValueError("view tables must both be [batch][view_stride]")
+    if view_token_mask is not None:
+        _dev(view_token_mask, "view_token_mask", torch.int32, 2)
+        if view_token_mask.shape != view_block_table.shape:
+            raise ValueError("view_token_mask must be shaped like the view tables")
+    nbytes = decode_schedule_bytes(kv, B, max_view_blocks)
+    with torch.cuda.stream(stream):
+        if out is None:
+            out = torch.empty(nbytes // 4, dtype=torch.int32, device=seq_lens.device)
+    if nbytes:
+        _dev(out, "out", torch.int32, 1)
+    if out.numel() * 4 < nbytes:
+        raise ValueError(f"out must hold {nbytes} bytes")
+    args = (ctypes.byref(kv.struct), B, _ptr(seq_lens), _ptr(view_block_table),
+            _ptr(view_logical_block), _ptr(view_token_mask), view_block_table.shape[1],
+            _ptr(view_num_blocks), int(max_view_blocks), _ptr(out) if out.numel() else None,
+            out.numel() * 4, _stream(stream))
+    return args, out
+
+
+def decode_schedule(kv: KVCache, seq_lens, view_block_table, view_logical_block,
+                    view_num_blocks, max_view_blocks: int, *, view_token_mask=None, out=None,
+                    stream=None):
+    """kap_decode_schedule: the balanced split assignment of decode calls on
+    this view, computed once. Returns an int32 tensor to pass as ``schedule``
+    (empty when these calls take no balanced map); written into ``out`` when
+    given."""
+    args, out = _schedule_call(kv, seq_lens, view_block_table, view_logical_block,
+                               view_num_blocks, max_view_blocks, view_token_mask, out, stream)
+    _check(load_library().kap_decode_schedule(*args))
+    return out
+
+
+def bind_decode_schedule(kv: KVCache, seq_lens, view_block_table, view_logical_block,
+                         view_num_blocks, max_view_blocks: int, out, view_token_mask=None,
+                         stream=None) -> "BoundCall":
+    """decode_schedule pre-marshalled (and run once here) for tight loops and
+    graph capture; each call rewrites ``out`` from the view arrays' current
+    contents."""
+    args, out = _schedule_call(kv, seq_lens, view_block_table, view_logical_block,
+                               view_num_blocks, max_view_blocks, view_token_mask, out, stream)
+    lib = load_library()
+    _check(lib.kap_decode_schedule(*args))
+    return BoundCall(lib.kap_decode_schedule, args,
+                     (kv, seq_lens, view_block_table, view_logical_block, view_num_blocks,
+                      view_token_mask, out))
 
 
 def selected_decode_noalloc(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
@@ -647,14 +736,15 @@ class BoundCall:
 def bind_selected_decode(kv: KVCache, q, seq_lens, view_block_table, view_logical_block,
                          view_num_blocks, max_view_blocks: int, sm_scale: float, out, lse,
                          workspace=None, num_splits: int = 0, view_token_mask=None,
-                         stream=None) -> BoundCall:
+                         schedule=None, stream=None) -> BoundCall:
     need = selected_decode_workspace_bytes(kv, q.shape[0], max_view_blocks, num_splits)
     have = 0 if workspace is None else workspace.numel() * workspace.element_size()
     if need > have:
         raise ValueError(f"workspace of {need} bytes required")
     fn, args, _, keep = _decode_call(kv, q, seq_lens, view_block_table, view_logical_block,
                                      view_num_blocks, max_view_blocks, sm_scale, num_splits,
-                                     out, lse, workspace, view_token_mask, stream)
+                                     out, lse, workspace, view_token_mask, stream,
+                                     schedule=schedule)
     _check(fn(*args))                                             # validates once
     return BoundCall(fn, args, keep)
 
