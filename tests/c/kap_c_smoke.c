@@ -7,9 +7,9 @@
  *   kap_c_smoke gpu   the worked plan vector of the selection rule (L = 100,
  *                     FBT = [7,3,9,0,5,2,8], spans (20,10,.5) (40,30,.9)
  *                     (90,5,.9) (0,5,.1), prefix 16, suffix 8, budget 60) in
- *                     page and token mode under both policies, and decode /
- *                     verify over one visible token, whose closed form is
- *                     out = v and lse = sm_scale * <q, k>
+ *                     page and token mode under both policies, and decode,
+ *                     scheduled decode and verify over one visible token,
+ *                     whose closed form is out = v and lse = sm_scale * <q, k>
  *
  * Prints one line per check and exits non-zero on the first failure.
  */
@@ -179,13 +179,27 @@ static void one_token(void) {
   if (need_v > need) need = need_v;
   HIP_OK(hipMalloc(&ws, need + 256));
   HIP_OK(hipMemset(ws, 0, need + 256));
+  /* the decode schedule of this view: the call refuses to run without it */
+  const size_t sched_bytes = kap_decode_schedule_bytes(&kv, 1, 1);
+  CHECK(sched_bytes > 0, "no schedule for a balanced decode");
+  int32_t *dsched = NULL;
+  HIP_OK(hipMalloc((void **)&dsched, sched_bytes));
+  CHECK(kap_selected_decode_scheduled(&kv, 1, dq, dt, dt + 1, dt + 2, NULL, 1, dt + 3, 1, NULL,
+                                      scale, dout, dlse, ws, need + 256, NULL) ==
+            KAP_ERR_INVALID_ARGUMENT, "scheduled decode without a schedule accepted");
+  CHECK(kap_decode_schedule(&kv, 1, dt, dt + 1, dt + 2, NULL, 1, dt + 3, 1, dsched, sched_bytes,
+                            NULL) == KAP_OK, "decode_schedule: %s", kap_last_error());
+  static const char *names[3] = {"decode", "verify", "scheduled decode"};
   float out[HQ * D], lse[HQ];
-  for (int call = 0; call < 2; ++call) {
+  for (int call = 0; call < 3; ++call) {
     kap_status s = call == 0
         ? kap_selected_decode(&kv, 1, dq, dt, dt + 1, dt + 2, 1, dt + 3, 1, scale, 0, dout, dlse,
                               ws, need + 256, NULL)
-        : kap_verify(&kv, 1, 1, dq, dt, dt + 1, 1, 1, scale, 0, dout, dlse, ws, need + 256, NULL);
-    CHECK(s == KAP_OK, "%s: %s", call ? "verify" : "decode", kap_last_error());
+        : call == 1
+        ? kap_verify(&kv, 1, 1, dq, dt, dt + 1, 1, 1, scale, 0, dout, dlse, ws, need + 256, NULL)
+        : kap_selected_decode_scheduled(&kv, 1, dq, dt, dt + 1, dt + 2, NULL, 1, dt + 3, 1,
+                                        dsched, scale, dout, dlse, ws, need + 256, NULL);
+    CHECK(s == KAP_OK, "%s: %s", names[call], kap_last_error());
     HIP_OK(hipDeviceSynchronize());
     HIP_OK(hipMemcpy(out, dout, sizeof out, hipMemcpyDeviceToHost));
     HIP_OK(hipMemcpy(lse, dlse, sizeof lse, hipMemcpyDeviceToHost));
@@ -194,13 +208,14 @@ static void one_token(void) {
       for (int d = 0; d < D; ++d) z += (double)qf[h][d] * kf[d];
       z *= scale;
       CHECK(fabs(lse[h] - z) <= 1e-5 * (1.0 + fabs(z)), "%s head %d lse %g, want %g",
-            call ? "verify" : "decode", h, lse[h], z);
+            names[call], h, lse[h], z);
       for (int d = 0; d < D; ++d)
         CHECK(fabs(out[h * D + d] - vf[d]) <= 1e-6, "%s head %d dim %d: %g, want %g",
-              call ? "verify" : "decode", h, d, out[h * D + d], vf[d]);
+              names[call], h, d, out[h * D + d], vf[d]);
     }
-    printf("ok one visible token (%s)\n", call ? "verify" : "decode");
+    printf("ok one visible token (%s)\n", names[call]);
   }
+  hipFree(dsched);
   hipFree(dk);
   hipFree(dv);
   hipFree(dq);

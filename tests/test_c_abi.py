@@ -27,4 +27,5 @@ def test_c_program_validation():
 @pytest.mark.gpu
 def test_c_program_on_the_gpu():
     out = run("gpu")
-    assert out.count("ok plan vector") == 4 and out.count("ok one visible token") == 2
+    assert out.count("ok plan vector") == 4 and out.count("ok one visible token") == 3
+    assert "ok one visible token (scheduled decode)" in out
