@@ -69,11 +69,11 @@ constexpr int kRowRor8 = 0x128;
 
 __device__ __forceinline__ float xor16_max(float x) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
-  return fmaxf(__int_as_float(r[0]), __int_as_float(r[1]));
+  return max_f(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 __device__ __forceinline__ float xor32_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
-  return fmaxf(__int_as_float(r[0]), __int_as_float(r[1]));
+  return max_f(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 __device__ __forceinline__ float xor16_sum(float x) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
@@ -369,11 +369,11 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
     s = ((vis >> t) & 1u) ? s * ksc : -INFINITY;
 
     // ---- online softmax ------------------------------------------------------
-    float pm = fmaxf(s, dpp<kQuadXor1>(s));
-    pm = fmaxf(pm, dpp<kQuadXor2>(pm));
+    float pm = max_f(s, dpp<kQuadXor1>(s));
+    pm = max_f(pm, dpp<kQuadXor2>(pm));
     pm = xor16_max(pm);
     pm = xor32_max(pm);
-    const float m_new = fmaxf(m_c, pm);
+    const float m_new = max_f(m_c, pm);
     if (__any(m_new > m_c)) {
       const float alpha = exp2_fast(m_c - (m_new == -INFINITY ? 0.f : m_new));
       l_c *= alpha;

@@ -116,10 +116,10 @@ constexpr int kMinChunkVerify = 8;
 int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
 // Resident workgroups per CU of a tuned kernel (cached per device).
-// id: 0/1 = decode bf16/fp8; 2 + 4*fp8 + (nt-1) = verify.
+// id: 0/1 = decode bf16/fp8; 2 + 8*c4 + 4*fp8 + (nt-1) = verify (c4: q_len % 4 == 1).
 int blocks_per_cu(int id, int kv_type, int q_len) {
   static std::mutex mu;
-  static int cache[64][10] = {{0}};
+  static int cache[64][18] = {{0}};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   std::lock_guard<std::mutex> lock(mu);
@@ -200,7 +200,8 @@ SplitPlan plan_verify(const kap_kv_cache *kv, int batch, int q_len, int max_page
     } else {
       const int fp8 = kv->kv_dtype == KAP_DT_FP8_E4M3FN;
       const int nt = (q_len * 4 + 15) / 16;
-      int bpc = blocks_per_cu(2 + 4 * fp8 + (nt - 1), fp8 ? kap::kFP8 : kap::kBF16, q_len);
+      int bpc = blocks_per_cu(2 + 8 * (q_len % 4 == 1) + 4 * fp8 + (nt - 1),
+                              fp8 ? kap::kFP8 : kap::kBF16, q_len);
       if (bpc <= 0) bpc = 1;
       if (units >= 4LL * kVerifyTargetPerCU * bpc * device_cus()) {
         p.n_split = 1;

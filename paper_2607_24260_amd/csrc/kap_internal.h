@@ -276,6 +276,14 @@ __device__ __forceinline__ kv_u32x2 fp8x4_to_bf16x4(uint32_t w) {
 // weights, whose sum is at least 1.
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// max(x, y) as the hardware maximum: unlike fmaxf it does not quiet signalling
+// NaNs first (one instruction per operand whose origin the compiler cannot
+// vouch for), and a NaN operand gives NaN -- which the softmax turns into NaN
+// outputs either way. Equal for all other inputs (+0 above -0).
+__device__ __forceinline__ float max_f(float x, float y) {
+  return __builtin_elementwise_maximum(x, y);
+}
+
 // One E4M3FN code -> float (generic path).
 __device__ __forceinline__ float fp8_to_f32(uint8_t b) {
   return __builtin_amdgcn_cvt_f32_fp8(static_cast<int>(b), 0);

@@ -48,11 +48,11 @@ __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) {
 
 __device__ __forceinline__ float xor16_max(float x) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
-  return fmaxf(__int_as_float(r[0]), __int_as_float(r[1]));
+  return max_f(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 __device__ __forceinline__ float xor32_max(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
-  return fmaxf(__int_as_float(r[0]), __int_as_float(r[1]));
+  return max_f(__int_as_float(r[0]), __int_as_float(r[1]));
 }
 __device__ __forceinline__ float xor16_sum(float x) {
   auto r = __builtin_amdgcn_permlane16_swap(__float_as_int(x), __float_as_int(x), false, false);
@@ -61,6 +61,28 @@ __device__ __forceinline__ float xor16_sum(float x) {
 __device__ __forceinline__ float xor32_sum(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(__float_as_int(x), __float_as_int(x), false, false);
   return __int_as_float(r[0]) + __int_as_float(r[1]);
+}
+
+// Moves within each 16-lane row (DPP): lane i of a row reads lane i - N
+// (row_shr), i + N (row_shl) or (i - N) mod 16 (row_ror) of the same row.
+constexpr int kRowShl(int n) { return 0x100 + n; }
+constexpr int kRowShr(int n) { return 0x110 + n; }
+constexpr int kRowRor(int n) { return 0x120 + n; }
+// src moved by CTRL into the lanes of the 4-lane banks set in BANKS (bank b =
+// lanes 4b .. 4b + 3 of every row); the other lanes keep old
+template <int CTRL, int BANKS>
+__device__ __forceinline__ float dpp_into(float old, float src) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(src), CTRL,
+                                                    0xF, BANKS, false));
+}
+// x moved by CTRL in every lane; a lane whose source lies outside its row reads 0
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_all(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_all(float x) {
+  return __uint_as_float(dpp_all<CTRL>(__float_as_uint(x)));
 }
 
 __device__ __forceinline__ uint32_t pack_bf16_exact(float lo, float hi) {
@@ -210,7 +232,12 @@ constexpr int kVerifyWaves = 4;
 // runs two per SIMD (asking for it explicitly cost 1%).
 constexpr int verify_min_waves(int kv, int nt) { return kv == kFP8 && (nt == 2 || nt == 3) ? 2 : 1; }
 
-template <int KV, int NT>
+// C4: the last row tile holds a single window token (q_len = 4 (NT - 1) + 1),
+// i.e. 4 of its 16 rows are real. Its softmax then runs on the 4 x 32 logits
+// gathered into all 64 lanes (two per lane) instead of on all 16 rows, which
+// removes about 30 vector instructions per page pair and KV head; the
+// weights return to the P^T operand layout for the products.
+template <int KV, int NT, bool C4>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(verify_min_waves(KV, NT))))
 void verify_mfma_kernel(AttnArgs a) {
   __shared__ float s_acc[kVerifyWaves][16][kD + 4];
@@ -290,6 +317,9 @@ void verify_mfma_kernel(AttnArgs a) {
     for (int dt = 0; dt < 8; ++dt) acc[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   const int last_full = (L - a.q_len) / kPage;   // pages below this are fully visible to all rows
+  // C4 tile: rows 16 (NT - 1) .. + 3 are the four heads of window token
+  // 4 (NT - 1), which sees logical positions below lim_c4
+  const int lim_c4 = L - a.q_len + 4 * (NT - 1) + 1;
 
   // RING pair buffers (windows of up to 8 tokens: two -- three were 0.2-0.5%
   // slower for bf16 on MI355X, e.g. 333.0 vs 331.9 us at 128K; 9..12-token
@@ -372,6 +402,58 @@ void verify_mfma_kernel(AttnArgs a) {
     u32x4 phi[NT], plo[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
+      if constexpr (C4) {
+        if (nt == NT - 1) {
+          // Lane (j, n < 4) holds row n's keys 4j .. 4j+3 of both pages. Gather
+          // them into lane 16 j + 4 c + n: c = 0, 1 take keys 4j + 2c, + 1 of
+          // page A; c = 2, 3 keys 4j + 2(c - 2), + 1 of page B. Row n's 32
+          // logits then sit two per lane in the 16 lanes with lane % 4 = n.
+          float c0 = sA[nt][0], c1 = sA[nt][1];
+          c0 = dpp_into<kRowShr(4), 0x2>(c0, sA[nt][2]);
+          c1 = dpp_into<kRowShr(4), 0x2>(c1, sA[nt][3]);
+          c0 = dpp_into<kRowShr(8), 0x4>(c0, sB[nt][0]);
+          c1 = dpp_into<kRowShr(8), 0x4>(c1, sB[nt][1]);
+          c0 = dpp_into<kRowShr(12), 0x8>(c0, sB[nt][2]);
+          c1 = dpp_into<kRowShr(12), 0x8>(c1, sB[nt][3]);
+          const bool onB = (lane & 8) != 0;
+          const float ksc = onB ? kscB : kscA;
+          float z0 = c0 * ksc, z1 = c1 * ksc;
+          if (needs_mask) {
+            const int pos = (k + (onB ? 1 : 0)) * kPage + 4 * j + 2 * ((lane >> 2) & 1);
+            const bool ok = onB ? okB : okA;
+            if (!ok || pos >= lim_c4) z0 = -INFINITY;
+            if (!ok || pos + 1 >= lim_c4) z1 = -INFINITY;
+          }
+          float mx = max_f(z0, z1);
+          mx = max_f(mx, dpp_all<kRowRor(4)>(mx));
+          mx = max_f(mx, dpp_all<kRowRor(8)>(mx));
+          mx = xor16_max(mx);
+          mx = xor32_max(mx);
+          // every lane now holds the running state of row lane % 4, which
+          // for the accumulator lanes (j, n < 4) is their own row
+          const float m_new = max_f(m[nt], mx);
+          const float mref = (m_new == -INFINITY) ? 0.f : m_new;
+          if (m_new > m[nt]) {
+            const float alpha = exp2_fast(m[nt] - mref);
+            l[nt] *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) acc[nt][dt] *= alpha;
+            m[nt] = m_new;
+          }
+          const float p0 = exp2_fast(z0 - mref), p1 = exp2_fast(z1 - mref);
+          l[nt] += p0 + p1;
+          const float vsc = onB ? vscB : vscA;
+          const float pv0 = p0 * vsc, pv1 = p1 * vsc;
+          const float pl0 = pv0 - __uint_as_float(__float_as_uint(pv0) & 0xffff0000u);
+          const float pl1 = pv1 - __uint_as_float(__float_as_uint(pv1) & 0xffff0000u);
+          const uint32_t h = pack_bf16_exact(pv0, pv1), lw = pack_bf16_exact(pl0, pl1);
+          // back to lane (j, n): the pieces of lanes 16 j + 4 c + n, c = 0..3
+          phi[nt] = u32x4{h, dpp_all<kRowShl(4)>(h), dpp_all<kRowShl(8)>(h), dpp_all<kRowShl(12)>(h)};
+          plo[nt] = u32x4{lw, dpp_all<kRowShl(4)>(lw), dpp_all<kRowShl(8)>(lw),
+                          dpp_all<kRowShl(12)>(lw)};
+          continue;
+        }
+      }
       float z[8];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -389,10 +471,10 @@ void verify_mfma_kernel(AttnArgs a) {
       }
       float mx = z[0];
 #pragma unroll
-      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, z[e]);
+      for (int e = 1; e < 8; ++e) mx = max_f(mx, z[e]);
       mx = xor16_max(mx);
       mx = xor32_max(mx);
-      const float m_new = fmaxf(m[nt], mx);
+      const float m_new = max_f(m[nt], mx);
       const float mref = (m_new == -INFINITY) ? 0.f : m_new;
       if (m_new > m[nt]) {
         const float alpha = exp2_fast(m[nt] - mref);
@@ -493,7 +575,12 @@ void verify_mfma_kernel(AttnArgs a) {
   // ---- combine the four wavefronts, tile by tile, then write ----------------------
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    float lt = xor16_sum(l[nt]);
+    float lt = l[nt];
+    if (C4 && nt == NT - 1) {   // the gathered tile's sums are spread over lane bits 2, 3 too
+      lt += dpp_all<kRowRor(4)>(lt);
+      lt += dpp_all<kRowRor(8)>(lt);
+    }
+    lt = xor16_sum(lt);
     lt = xor32_sum(lt);
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt)
@@ -565,29 +652,46 @@ void verify_mfma_kernel(AttnArgs a) {
     merge_rows(a, b, g, R, wi.slot0, n_split);
 }
 
+// q_len -> row tiles, and whether the last tile holds a single window token
+constexpr bool c4_window(int q_len) { return q_len % 4 == 1; }
+
+template <int KV, int NT>
+void launch_nt(const AttnArgs &a, dim3 grid, hipStream_t s) {
+  if (c4_window(a.q_len))
+    hipLaunchKernelGGL((verify_mfma_kernel<KV, NT, true>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((verify_mfma_kernel<KV, NT, false>), grid, dim3(256), 0, s, a);
+}
+
 template <int KV>
 hipError_t launch_kv(const AttnArgs &a, hipStream_t s) {
   const dim3 grid = a.ragged ? dim3(a.n_split) : dim3(a.n_split, a.Hkv, a.batch);
   const int nt = (a.q_len * 4 + 15) / 16;
   switch (nt) {
-    case 1: hipLaunchKernelGGL((verify_mfma_kernel<KV, 1>), grid, dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((verify_mfma_kernel<KV, 2>), grid, dim3(256), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((verify_mfma_kernel<KV, 3>), grid, dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((verify_mfma_kernel<KV, 4>), grid, dim3(256), 0, s, a); break;
+    case 1: launch_nt<KV, 1>(a, grid, s); break;
+    case 2: launch_nt<KV, 2>(a, grid, s); break;
+    case 3: launch_nt<KV, 3>(a, grid, s); break;
+    case 4: launch_nt<KV, 4>(a, grid, s); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+template <int KV, int NT>
+hipError_t occupancy_nt(int *nb, bool c4) {
+  return c4 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(nb, verify_mfma_kernel<KV, NT, true>, 256, 0)
+            : hipOccupancyMaxActiveBlocksPerMultiprocessor(nb, verify_mfma_kernel<KV, NT, false>, 256, 0);
+}
+
 template <int KV>
-int blocks_kv(int nt) {
+int blocks_kv(int nt, bool c4) {
   int nb = 0;
   hipError_t e = hipErrorInvalidValue;
   switch (nt) {
-    case 1: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 1>, 256, 0); break;
-    case 2: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 2>, 256, 0); break;
-    case 3: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 3>, 256, 0); break;
-    case 4: e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, verify_mfma_kernel<KV, 4>, 256, 0); break;
+    case 1: e = occupancy_nt<KV, 1>(&nb, c4); break;
+    case 2: e = occupancy_nt<KV, 2>(&nb, c4); break;
+    case 3: e = occupancy_nt<KV, 3>(&nb, c4); break;
+    case 4: e = occupancy_nt<KV, 4>(&nb, c4); break;
     default: break;
   }
   return e == hipSuccess ? nb : 0;
@@ -603,7 +707,8 @@ hipError_t launch_verify_mfma(const AttnArgs &a, hipStream_t s) {
 
 int verify_mfma_blocks_per_cu(int kv_type, int q_len) {
   const int nt = (q_len * 4 + 15) / 16;
-  return kv_type == kFP8 ? blocks_kv<kFP8>(nt) : blocks_kv<kBF16>(nt);
+  const bool c4 = c4_window(q_len);
+  return kv_type == kFP8 ? blocks_kv<kFP8>(nt, c4) : blocks_kv<kBF16>(nt, c4);
 }
 
 }  // namespace kap
