@@ -283,6 +283,38 @@ def test_verify_window_sizes_ragged_fp8(q_len):
     assert_close("LSE", lse.cpu().numpy(), el, LSE_TOL)
 
 
+@pytest.mark.parametrize("q_len", [1, 5, 9, 13, 16])
+def test_fp8_page_scales_of_any_sign_and_size(q_len):
+    """Per-page fp8 scales are plain floats: a negative K scale flips a page's
+    logits, a zero K scale makes them 0 and a zero V scale blanks the page's
+    values; K scales up to 16x and V scales down to 2^-8 of the quantiser's.
+    Pages of different sign and size share a page pair, so the fold of the
+    scales into logits and weights is checked per page -- also in the
+    gathered last row tile of 1-, 5-, 9- and 13-token windows."""
+    w, _ = workload(5, batch=4, seq_len=5000, n_decode=1, n_verify=1)
+    _CACHE.clear()                  # the workload's scales are changed below
+    sc = w.kv_scales[0]
+    gen = torch.Generator(device="cuda").manual_seed(1000 + q_len)
+    kf = torch.tensor([1.0, -1.0, 0.0, 0.25, 4.0, 16.0, -3.0], device="cuda")
+    vf = torch.tensor([1.0, -1.0, 0.0, 0.25, 2.0 ** -8, 4.0, -2.0], device="cuda")
+    n = sc.shape[0]
+    sc[:, 0] *= kf[torch.randint(0, len(kf), (n,), generator=gen, device="cuda")]
+    sc[:, 1] *= vf[torch.randint(0, len(vf), (n,), generator=gen, device="cuda")]
+    torch.cuda.synchronize()
+    pool = oracle_pool(w)
+    lens = np.array([4000, 3999, 37, q_len], dtype=np.int32)
+    g = torch.Generator(device="cuda").manual_seed(200 + q_len)
+    q = (torch.randn((4, q_len, 32, 128), generator=g, device="cuda") / 11.3).to(torch.bfloat16)
+    o, lse = K.verify(kv_of(w), q, dev_i32(lens), dev_i32(w.full_block_table), 4000, 1.0)
+    torch.cuda.synchronize()
+    eo, el = O.verify(pool, q.float().cpu().numpy(), lens, w.full_block_table, 1.0)
+    assert_close("verify O", o.cpu().numpy(), eo, O_TOL)
+    assert_close("verify LSE", lse.cpu().numpy(), el, LSE_TOL)
+    if q_len == 1:
+        decode_check(w, pool, [0])
+        decode_check(w, pool, [0], num_splits=3)
+
+
 def test_window_longer_than_sequence_gives_empty_rows():
     w, pool = workload(2, batch=2, seq_len=100, n_decode=1, n_verify=1)
     w.seq_lens[:] = [3, 100]
