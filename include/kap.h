@@ -17,6 +17,14 @@
  *                        full paged KV cache (Sec. 3.2, "Full-context
  *                        verification"; Eq. (2)).
  *
+ * Around them: kap_decode_schedule writes, once per view, the split map that
+ * kap_selected_decode_scheduled then reads instead of computing it in every
+ * proposal step (the view is fixed across the k steps of a cycle);
+ * kap_selected_decode_masked takes token-granular views; kap_append_kv and
+ * kap_compact_view maintain the pool; kap_fallback_update switches sequences
+ * to full-context access (Sec. 3.2, "Runtime stability and fallback");
+ * kap_accept_top3 scores draft windows.
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Every array argument is device memory owned by the caller. The library
