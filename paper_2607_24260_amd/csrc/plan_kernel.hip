@@ -4,9 +4,10 @@
 // Per sequence the workgroup
 //   1. checks the CSR bounds, the length and the scores (status codes),
 //   2. marks the mandatory prefix / suffix in an LDS bitmap,
-//   3. ranks the spans by (prior desc, start asc, index asc) -- every thread
-//      counts, for its spans, how many spans precede them, and writes the
-//      inverse permutation to the workspace,
+//   3. ranks the spans by (prior desc, start asc, index asc) -- for every
+//      span, 1 to 8 threads (as many as the span count leaves) count how many
+//      spans precede it, and the inverse permutation goes to LDS (to the
+//      workspace when the spans exceed one LDS chunk),
 //   4. walks the spans in rank order with one wavefront, 64 at a time: each
 //      lane prices its span against the bitmap (its cost in visible tokens),
 //      a ballot finds the first span that fits, and only a taken span changes
@@ -65,6 +66,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __shared__ int s_taken;
   __shared__ __align__(16) float s_prior[kRankChunk];
   __shared__ __align__(16) int s_start[kRankChunk];
+  __shared__ int s_perm[kRankChunk];   // one chunk: rank -> local span index
 
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
@@ -125,6 +127,15 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     write_fail(2 /*KAP_PLAN_BAD_SCORE*/, true);
     return;
   }
+  // one chunk: the span lengths the greedy walk needs, loaded now and stored
+  // to LDS (over the priors) once the ranking is done
+  constexpr int kLenRegs = kRankChunk / kPlanThreads;
+  int len_r[kLenRegs];
+#pragma unroll
+  for (int q = 0; q < kLenRegs; ++q) {
+    const int t = tid + q * kPlanThreads;
+    len_r[q] = (one_chunk && t < n) ? a.span_len[lo + t] : 0;
+  }
 
   // -- mandatory prefix / suffix ----------------------------------------------
   const int pre = min(max(a.prefix[b], 0), L);
@@ -147,9 +158,13 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   // -- rank the spans ---------------------------------------------------------
   // rank(i) = number of spans ordered before span i; keys are read from LDS in
   // chunks of kRankChunk (a single chunk, staged above, in the common case),
-  // four per broadcast read.
-  for (int ib = 0; ib < n; ib += kPlanThreads) {
-    const int i = ib + tid;
+  // four per broadcast read. With few spans, TS = 2, 4 or 8 neighbouring
+  // threads share span i, thread s counting over keys 4 s, 4 s + 4 TS, ...,
+  // and their counts are summed with lane swaps.
+  const int TS = n <= kPlanThreads / 8 ? 8 : n <= kPlanThreads / 4 ? 4 : n <= kPlanThreads / 2 ? 2 : 1;
+  const int sub = tid & (TS - 1);
+  for (int ib = 0; ib < n; ib += kPlanThreads / TS) {
+    const int i = ib + tid / TS;
     const bool act = i < n;
     float pi = 0.f;
     int si = 0;
@@ -172,7 +187,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
       }
       if (act) {
 #pragma unroll 4
-        for (int t = 0; t < jn4; t += 4) {
+        for (int t = 4 * sub; t < jn4; t += 4 * TS) {
           const float4 p4 = *reinterpret_cast<const float4 *>(&s_prior[t]);
           const int4 s4 = *reinterpret_cast<const int4 *>(&s_start[t]);
           const int j = jb + t;
@@ -181,9 +196,21 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
         }
       }
     }
-    if (act) {
-      a.perm[lo + rank] = i;
+    // the TS threads of span i are lanes l .. l + TS - 1 of one wavefront
+    for (int m = 1; m < TS; m <<= 1) rank += __shfl_xor(rank, m);
+    if (act && sub == 0) {
+      if (one_chunk) s_perm[rank] = i;
+      else a.perm[lo + rank] = i;
       if (a.span_selected) a.span_selected[lo + i] = 0;
+    }
+  }
+  __syncthreads();
+  int *s_len = reinterpret_cast<int *>(s_prior);   // the priors are no longer needed
+  if (one_chunk) {
+#pragma unroll
+    for (int q = 0; q < kLenRegs; ++q) {
+      const int t = tid + q * kPlanThreads;
+      if (t < n) s_len[t] = len_r[q];
     }
   }
   __syncthreads();
@@ -227,10 +254,11 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     for (int r0 = 0; r0 < n && !stop; r0 += 64) {
       int my_i = -1, x = 0, e = 0;
       if (r0 + lane < n) {
-        my_i = lo + a.perm[lo + r0 + lane];
-        const long long st = a.span_start[my_i];
+        const int li = one_chunk ? s_perm[r0 + lane] : a.perm[lo + r0 + lane];
+        my_i = lo + li;
+        const long long st = one_chunk ? s_start[li] : a.span_start[my_i];
         const long long x64 = st > 0 ? st : 0;
-        long long e64 = st + (long long)a.span_len[my_i];
+        long long e64 = st + (long long)(one_chunk ? s_len[li] : a.span_len[my_i]);
         if (e64 > L) e64 = L;
         x = (int)x64;
         e = (int)(e64 > x64 ? e64 : x64);               // e <= x: empty after clipping
