@@ -26,11 +26,16 @@ namespace {
 
 constexpr int kRankChunk = 2048;   // ranking keys staged per pass; also the LDS view list
 
-// Branch-free: equal priors (including -0 == +0) fall through to the start,
-// then to the index.
-__device__ __forceinline__ int ranks_before(float pj, int sj, int j, float pi, int si, int i) {
-  return (pj > pi) | ((pj == pi) & ((sj < si) | ((sj == si) & (j < i))));
+// The ranking order without the index, as one unsigned integer: the prior,
+// descending (-0 ranks as +0; NaN never gets here), above the start,
+// ascending. Span j ranks before span i iff key_j < key_i, or the keys are
+// equal and j < i. No span's key is ~0 (the padding key).
+__device__ __forceinline__ uint64_t rank_key(float prior, int start) {
+  uint32_t u = __float_as_uint(prior == 0.f ? 0.f : prior);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);   // monotone in the float's value
+  return ((uint64_t)~u << 32) | (uint32_t)(start ^ 0x80000000);
 }
+constexpr uint64_t kPadKey = ~0ull;
 
 // Exclusive prefix sum of v over the workgroup (kPlanThreads threads, in
 // thread order); *total receives the sum. s_tmp holds kPlanThreads/64 ints.
@@ -64,8 +69,16 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   __shared__ int s_scan[kPlanThreads / 64];
   __shared__ long long s_used;
   __shared__ int s_taken;
-  __shared__ __align__(16) float s_prior[kRankChunk];
-  __shared__ __align__(16) int s_start[kRankChunk];
+  // ranking keys; after the ranking (one chunk) each span's (length, start);
+  // at the end the view list (and its token masks)
+  __shared__ __align__(16) union {
+    uint64_t key[kRankChunk];
+    struct {
+      int page[kRankChunk];
+      uint32_t mask[kRankChunk];
+    } view;
+  } s_u;
+  uint64_t *const s_key = s_u.key;
   __shared__ int s_perm[kRankChunk];   // one chunk: rank -> local span index
 
   const int b = blockIdx.x;
@@ -99,8 +112,8 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   }
 
   // -- scores, and the first chunk of ranking keys -----------------------------
-  // Keys are staged in LDS padded to a multiple of four with keys that rank
-  // after every span (prior -inf, start INT_MAX, index >= n).
+  // Keys are staged in LDS padded to a multiple of four with the padding key,
+  // which no span's key equals or exceeds.
   const int n = hi - lo;
   const bool one_chunk = n <= kRankChunk;
   if (tid == 0) s_flag = 0;
@@ -112,13 +125,9 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
       if (t < n) {
         const float pr = a.span_prior[lo + t];
         if (__builtin_isnan(pr)) s_flag = 1;
-        if (t < kRankChunk) {
-          s_prior[t] = pr;
-          s_start[t] = a.span_start[lo + t];
-        }
+        if (t < kRankChunk) s_key[t] = rank_key(pr, a.span_start[lo + t]);
       } else {
-        s_prior[t] = -INFINITY;
-        s_start[t] = 0x7fffffff;
+        s_key[t] = kPadKey;
       }
     }
   }
@@ -128,7 +137,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     return;
   }
   // one chunk: the span lengths the greedy walk needs, loaded now and stored
-  // to LDS (over the priors) once the ranking is done
+  // to LDS (beside the starts) once the ranking is done
   constexpr int kLenRegs = kRankChunk / kPlanThreads;
   int len_r[kLenRegs];
 #pragma unroll
@@ -156,48 +165,64 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   }
 
   // -- rank the spans ---------------------------------------------------------
-  // rank(i) = number of spans ordered before span i; keys are read from LDS in
-  // chunks of kRankChunk (a single chunk, staged above, in the common case),
-  // four per broadcast read. With few spans, TS = 2, 4 or 8 neighbouring
-  // threads share span i, thread s counting over keys 4 s, 4 s + 4 TS, ...,
-  // and their counts are summed with lane swaps.
+  // rank(i) = number of spans ordered before span i = #{j : key_j < key_i}
+  // + #{j < i : key_j = key_i}. Keys are read from LDS in chunks of
+  // kRankChunk (a single chunk, staged above, in the common case), four per
+  // two broadcast reads. One pass counts the keys below and equal to key_i;
+  // only when some span shares its key with another (equal prior and start)
+  // does a second pass count the equal keys of lower index. With few spans,
+  // TS = 2, 4 or 8 neighbouring threads share span i, thread s counting over
+  // keys 4 s, 4 s + 4 TS, ..., and their counts are summed with lane swaps.
   const int TS = n <= kPlanThreads / 8 ? 8 : n <= kPlanThreads / 4 ? 4 : n <= kPlanThreads / 2 ? 2 : 1;
   const int sub = tid & (TS - 1);
-  for (int ib = 0; ib < n; ib += kPlanThreads / TS) {
-    const int i = ib + tid / TS;
-    const bool act = i < n;
-    float pi = 0.f;
-    int si = 0;
-    if (act) {
-      pi = one_chunk ? s_prior[i] : a.span_prior[lo + i];
-      si = one_chunk ? s_start[i] : a.span_start[lo + i];
-    }
-    int rank = 0;
+  typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+  // counts over all chunks: below (ties == false) or equal with lower index
+  // (ties == true); every thread takes part (chunk staging has barriers)
+  auto count = [&](bool act, int i, uint64_t ki, bool ties, int &c_lt, int &c_eq) {
     for (int jb = 0; jb < n; jb += kRankChunk) {
       const int jn = min(kRankChunk, n - jb);
       const int jn4 = (jn + 3) & ~3;
       if (!one_chunk) {
         __syncthreads();
-        for (int t = tid; t < jn4; t += kPlanThreads) {
-          const bool real = t < jn;
-          s_prior[t] = real ? a.span_prior[lo + jb + t] : -INFINITY;
-          s_start[t] = real ? a.span_start[lo + jb + t] : 0x7fffffff;
-        }
+        for (int t = tid; t < jn4; t += kPlanThreads)
+          s_key[t] = t < jn ? rank_key(a.span_prior[lo + jb + t], a.span_start[lo + jb + t]) : kPadKey;
         __syncthreads();
       }
       if (act) {
-#pragma unroll 4
+#pragma unroll 2
         for (int t = 4 * sub; t < jn4; t += 4 * TS) {
-          const float4 p4 = *reinterpret_cast<const float4 *>(&s_prior[t]);
-          const int4 s4 = *reinterpret_cast<const int4 *>(&s_start[t]);
-          const int j = jb + t;
-          rank += ranks_before(p4.x, s4.x, j, pi, si, i) + ranks_before(p4.y, s4.y, j + 1, pi, si, i) +
-                  ranks_before(p4.z, s4.z, j + 2, pi, si, i) + ranks_before(p4.w, s4.w, j + 3, pi, si, i);
+          const u64x2 k01 = *reinterpret_cast<const u64x2 *>(&s_key[t]);
+          const u64x2 k23 = *reinterpret_cast<const u64x2 *>(&s_key[t + 2]);
+          if (!ties) {
+            c_lt += (k01.x < ki) + (k01.y < ki) + (k23.x < ki) + (k23.y < ki);
+            c_eq += (k01.x == ki) + (k01.y == ki) + (k23.x == ki) + (k23.y == ki);
+          } else {
+            const int j = jb + t;
+            c_eq += ((k01.x == ki) & (j < i)) + ((k01.y == ki) & (j + 1 < i)) +
+                    ((k23.x == ki) & (j + 2 < i)) + ((k23.y == ki) & (j + 3 < i));
+          }
         }
       }
     }
     // the TS threads of span i are lanes l .. l + TS - 1 of one wavefront
-    for (int m = 1; m < TS; m <<= 1) rank += __shfl_xor(rank, m);
+    for (int m = 1; m < TS; m <<= 1) {
+      c_lt += __shfl_xor(c_lt, m);
+      c_eq += __shfl_xor(c_eq, m);
+    }
+  };
+  for (int ib = 0; ib < n; ib += kPlanThreads / TS) {
+    const int i = ib + tid / TS;
+    const bool act = i < n;
+    uint64_t ki = kPadKey;
+    if (act) ki = one_chunk ? s_key[i] : rank_key(a.span_prior[lo + i], a.span_start[lo + i]);
+    int below = 0, equal = 0;
+    count(act, i, ki, false, below, equal);   // equal counts span i itself
+    int rank = below;
+    if (__syncthreads_or(act && equal > 1)) {
+      int unused = 0, tied = 0;
+      count(act, i, ki, true, unused, tied);
+      rank += tied;
+    }
     if (act && sub == 0) {
       if (one_chunk) s_perm[rank] = i;
       else a.perm[lo + rank] = i;
@@ -205,12 +230,12 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     }
   }
   __syncthreads();
-  int *s_len = reinterpret_cast<int *>(s_prior);   // the priors are no longer needed
   if (one_chunk) {
+    // (length, start) of every span for the greedy walk, over its key
 #pragma unroll
     for (int q = 0; q < kLenRegs; ++q) {
       const int t = tid + q * kPlanThreads;
-      if (t < n) s_len[t] = len_r[q];
+      if (t < n) s_key[t] = ((uint64_t)(uint32_t)len_r[q] << 32) | (uint32_t)(s_key[t] & 0xffffffffu);
     }
   }
   __syncthreads();
@@ -254,11 +279,28 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
     for (int r0 = 0; r0 < n && !stop; r0 += 64) {
       int my_i = -1, x = 0, e = 0;
       if (r0 + lane < n) {
-        const int li = one_chunk ? s_perm[r0 + lane] : a.perm[lo + r0 + lane];
+        // (two separate paths: merged into one load from a selected address,
+        // the LDS and the global read would both become generic loads)
+        int li;
+        if (one_chunk) {
+          li = s_perm[r0 + lane];
+        } else {
+          li = a.perm[lo + r0 + lane];
+          asm volatile("" ::: "memory");
+        }
         my_i = lo + li;
-        const long long st = one_chunk ? s_start[li] : a.span_start[my_i];
+        int st32, len32;
+        if (one_chunk) {
+          const uint64_t v = s_key[li];
+          st32 = (int)((uint32_t)v ^ 0x80000000u);
+          len32 = (int)(uint32_t)(v >> 32);
+        } else {
+          st32 = a.span_start[my_i];
+          len32 = a.span_len[my_i];
+        }
+        const long long st = st32;
         const long long x64 = st > 0 ? st : 0;
-        long long e64 = st + (long long)(one_chunk ? s_len[li] : a.span_len[my_i]);
+        long long e64 = st + (long long)len32;
         if (e64 > L) e64 = L;
         x = (int)x64;
         e = (int)(e64 > x64 ? e64 : x64);               // e <= x: empty after clipping
@@ -345,11 +387,10 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   // ... through the full block table, so the table reads are all in flight
   // at once. Longer views map each page where it is found.
   const bool staged = nblk <= kRankChunk;
-  uint32_t *s_lmask = reinterpret_cast<uint32_t *>(s_prior);
   auto emit = [&](int p, uint32_t mask) {
     if (staged) {
-      s_start[out] = p;
-      if constexpr (TOK) s_lmask[out] = mask;
+      s_u.view.page[out] = p;
+      if constexpr (TOK) s_u.view.mask[out] = mask;
     } else {
       const int page = fbt_row[p];
       bad |= (page < 0) || ((int64_t)page >= a.num_pages);
@@ -376,12 +417,12 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
   if (staged) {
     __syncthreads();
     for (int k = tid; k < nblk; k += kPlanThreads) {
-      const int p = s_start[k];
+      const int p = s_u.view.page[k];
       const int page = fbt_row[p];
       bad |= (page < 0) || ((int64_t)page >= a.num_pages);
       vlb[k] = p;
       vbt[k] = page;
-      if constexpr (TOK) vmk[k] = s_lmask[k];
+      if constexpr (TOK) vmk[k] = s_u.view.mask[k];
     }
   }
   if (bad) s_flag = 1;
