@@ -112,6 +112,28 @@ def test_many_spans_one_sequence():
     run_both([L], [rng.permutation(stride)], [spans], [512], [256], [9000])
 
 
+@pytest.mark.parametrize("n", [200, 2500])
+@pytest.mark.parametrize("policy", [0, 1])
+def test_spans_with_equal_prior_and_start(n, policy):
+    # many spans share both prior (0.0 and -0.0 are equal) and start (4
+    # starts), so their order is decided by their index alone; the lengths
+    # differ, and under STOP the reversed order gives other pages and other
+    # selected spans (checked with the oracle). 2500 spans take the
+    # multi-chunk ranking path.
+    rng = np.random.default_rng(95 + n)
+    L = 4000
+    stride = L // 16
+    starts = rng.choice(np.arange(0, 3600, 16), 4, replace=False)
+    spans = [(int(rng.choice(starts)), int(rng.integers(16, 800)),
+              float(rng.choice([0.0, -0.0, 1.0]))) for _ in range(n)]
+    fbt = rng.permutation(stride)
+    if policy == 1:
+        fw = O.compile_plan_one(L, fbt, *zip(*spans), 0, 1, 1600, 1, stride, stride)
+        rv = O.compile_plan_one(L, fbt, *zip(*spans[::-1]), 0, 1, 1600, 1, stride, stride)
+        assert list(fw.logical_blocks) != list(rv.logical_blocks)
+    run_both([L], [fbt], [spans], [0], [1], [1600], policy=policy)
+
+
 @pytest.mark.parametrize("config", [1, 2, 3, 4, 5])
 @pytest.mark.parametrize("policy", [0, 1])
 def test_workload_plans(config, policy):
