@@ -515,7 +515,7 @@ __global__ __launch_bounds__(256) void decode_fast_kernel(AttnArgs a) {
       partial_store1(rl, pr * 4, s_plse[threadIdx.x]);
     }
   }
-  if (last_arrival(a, b, g, n_split, &s_flag)) merge_rows(a, b, g, 4, wi.slot0, n_split);
+  if (last_arrival(a, b, g, n_split, &s_flag)) merge_rows<1>(a, b, g, 4, wi.slot0, n_split);
 }
 
 template <int KV, int RING, bool MASKED>

@@ -521,55 +521,84 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
 // LSE merge of the ns partials (slots slot0 .. slot0 + ns - 1) of the R_loc
 // local rows of (b, g), D = 128:
 // lse = log2 sum_s 2^lse_s, o = sum_s 2^(lse_s - lse) o_s (empty splits drop out).
-// The partials are read eight splits at a time with independent loads (one
-// memory round trip per eight splits) and folded in with a running maximum.
+// Every thread takes up to kMergeItems (row, 4-dim) items at once -- one for
+// decode's 4 rows (128 items), 3 for verify's up to 64 (one pass over 640
+// items at 20 rows instead of three) -- and reads their partials eight splits
+// at a time with independent loads (one memory round trip per eight splits
+// for all its items), folding them in with a running maximum.
+template <int kMergeItems>
 __device__ __forceinline__ void merge_rows(const AttnArgs &a, int b, int g, int R_loc, int slot0,
                                            int ns) {
   constexpr int kBatch = 8;
   const auto ro = partial_rsrc(a.part_o);
   const auto rl = partial_rsrc(a.part_lse);
-  for (int e = threadIdx.x; e < R_loc * 32; e += blockDim.x) {
-    const int r = e >> 5, d4 = (e & 31) * 4;
-    const size_t row = out_row(a, b, g, r);
-    float M = -INFINITY, tot = 0.f;
-    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int n_items = R_loc * 32;
+  for (int e0 = threadIdx.x; e0 < n_items; e0 += kMergeItems * blockDim.x) {
+    bool ok[kMergeItems];
+    int r[kMergeItems], d4[kMergeItems];
+    float M[kMergeItems], tot[kMergeItems];
+    float4 o[kMergeItems];
+#pragma unroll
+    for (int it = 0; it < kMergeItems; ++it) {
+      const int e = e0 + it * blockDim.x;
+      ok[it] = e < n_items;
+      r[it] = ok[it] ? e >> 5 : 0;
+      d4[it] = (e & 31) * 4;
+      M[it] = -INFINITY;
+      tot[it] = 0.f;
+      o[it] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
     for (int s0 = 0; s0 < ns; s0 += kBatch) {
-      float ls[kBatch];
-      float4 vs[kBatch];
+      float ls[kMergeItems][kBatch];
+      float4 vs[kMergeItems][kBatch];
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        const size_t pr = (size_t)(slot0 + min(s0 + j, ns - 1)) * R_loc + r;
-        ls[j] = partial_load1(rl, pr * 4);
-        vs[j] = partial_load4(ro, (pr * 128 + d4) * 4);
+      for (int it = 0; it < kMergeItems; ++it) {
+        if (!ok[it]) continue;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          const size_t pr = (size_t)(slot0 + min(s0 + j, ns - 1)) * R_loc + r[it];
+          ls[it][j] = partial_load1(rl, pr * 4);
+          vs[it][j] = partial_load4(ro, (pr * 128 + d4[it]) * 4);
+        }
       }
-      float mc = M;
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j)
-        if (s0 + j < ns) mc = fmaxf(mc, ls[j]);
-      if (mc == -INFINITY) continue;                 // every split so far is empty
-      const float sc = exp2f(M - mc);                // 0 while M is still -inf
-      tot *= sc;
-      o.x *= sc; o.y *= sc; o.z *= sc; o.w *= sc;
+      for (int it = 0; it < kMergeItems; ++it) {
+        if (!ok[it]) continue;
+        float mc = M[it];
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        if (s0 + j >= ns) continue;
-        const float w = exp2f(ls[j] - mc);
-        tot += w;
-        o.x = fmaf(w, vs[j].x, o.x);
-        o.y = fmaf(w, vs[j].y, o.y);
-        o.z = fmaf(w, vs[j].z, o.z);
-        o.w = fmaf(w, vs[j].w, o.w);
+        for (int j = 0; j < kBatch; ++j)
+          if (s0 + j < ns) mc = fmaxf(mc, ls[it][j]);
+        if (mc == -INFINITY) continue;               // every split so far is empty
+        const float sc = exp2f(M[it] - mc);          // 0 while M is still -inf
+        tot[it] *= sc;
+        o[it].x *= sc; o[it].y *= sc; o[it].z *= sc; o[it].w *= sc;
+#pragma unroll
+        for (int j = 0; j < kBatch; ++j) {
+          if (s0 + j >= ns) continue;
+          const float w = exp2f(ls[it][j] - mc);
+          tot[it] += w;
+          o[it].x = fmaf(w, vs[it][j].x, o[it].x);
+          o[it].y = fmaf(w, vs[it][j].y, o[it].y);
+          o[it].z = fmaf(w, vs[it][j].z, o[it].z);
+          o[it].w = fmaf(w, vs[it][j].w, o[it].w);
+        }
+        M[it] = mc;
       }
-      M = mc;
     }
-    float lse = -INFINITY;
-    if (M != -INFINITY) {
-      const float inv = 1.f / tot;
-      o.x *= inv; o.y *= inv; o.z *= inv; o.w *= inv;
-      lse = (M + log2f(tot)) * kLn2;
+#pragma unroll
+    for (int it = 0; it < kMergeItems; ++it) {
+      if (!ok[it]) continue;
+      const size_t row = out_row(a, b, g, r[it]);
+      float lse = -INFINITY;
+      float4 v = o[it];
+      if (M[it] != -INFINITY) {
+        const float inv = 1.f / tot[it];
+        v.x *= inv; v.y *= inv; v.z *= inv; v.w *= inv;
+        lse = (M[it] + log2f(tot[it])) * kLn2;
+      }
+      *reinterpret_cast<float4 *>(a.out + row * 128 + d4[it]) = v;
+      if (d4[it] == 0) a.lse[row] = lse;
     }
-    *reinterpret_cast<float4 *>(a.out + row * 128 + d4) = o;
-    if (d4 == 0) a.lse[row] = lse;
   }
 }
 

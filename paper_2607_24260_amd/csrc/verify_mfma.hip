@@ -649,7 +649,7 @@ void verify_mfma_kernel(AttnArgs a) {
 
   // ---- the last workgroup of (b, g) merges the splits ---------------------------------
   if (n_split > 1 && last_arrival(a, b, g, n_split, &s_flag))
-    merge_rows(a, b, g, R, wi.slot0, n_split);
+    merge_rows<3>(a, b, g, R, wi.slot0, n_split);
 }
 
 // q_len -> row tiles, and whether the last tile holds a single window token
