@@ -216,6 +216,22 @@ def test_split_count_does_not_change_result(kv_dtype):
         verify_check(w, pool, [0], num_splits=ns)
 
 
+@pytest.mark.parametrize("kv_dtype", ["bf16", "fp8"])
+def test_split_merge_of_long_windows(kv_dtype):
+    # 16-token windows: 64 rows, so the last workgroup merges 2048 (row, 4-dim)
+    # items, several per thread and in several passes; with the maximum split
+    # count every item folds in more than eight partials (several load batches)
+    cfg = 2 if kv_dtype == "bf16" else 5
+    w, pool = workload(cfg, batch=3, seq_len=5000, n_decode=1, n_verify=1)
+    orig = w.q_verify
+    try:
+        w.q_verify = [_window(w, 16, seed=16)]
+        for ns in (3, 10_000):
+            verify_check(w, pool, [0], num_splits=ns)
+    finally:
+        w.q_verify = orig
+
+
 def test_view_order_does_not_matter():
     w, pool = workload(2, batch=2, seq_len=4000, n_decode=1, n_verify=1)
     plan = gpu_plan(w)
