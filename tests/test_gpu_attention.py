@@ -331,6 +331,31 @@ def test_fp8_page_scales_of_any_sign_and_size(q_len):
         decode_check(w, pool, [0], num_splits=3)
 
 
+@pytest.mark.parametrize("seed", range(32))
+def test_random_shapes(seed):
+    """Seeded random batches: 1-6 sequences of 1-4096 tokens (partial pages,
+    sequences shorter than the window), random budgets per sequence, windows
+    of 1-16 tokens, bf16 or fp8, balanced or forced split counts; decode over
+    the plan's view and verify over the full table against the oracle."""
+    rng = np.random.default_rng(4242 + seed)
+    kv_dtype = "bf16" if seed % 2 == 0 else "fp8"
+    cfg = 2 if kv_dtype == "bf16" else 5
+    B = int(rng.integers(1, 7))
+    lens = [int(x) for x in rng.integers(1, 4097, B)]
+    w, pool = _ragged(cfg, B, 4096 if cfg == 2 else 5000, lens)
+    budget = np.array([int(rng.integers(0, L + 1)) for L in lens], dtype=np.int32)
+    ns = int(rng.choice([0, 0, 1, 2, 7, 10_000]))
+    decode_check(w, pool, [0], budget=budget, num_splits=ns)
+    q_len = int(rng.integers(1, 17))
+    q = _window(w, q_len, 900 + seed)
+    o, lse = K.verify(kv_of(w), q, dev_i32(w.seq_lens), dev_i32(w.full_block_table),
+                      int(max(lens)), 1.0, num_splits=ns)
+    torch.cuda.synchronize()
+    eo, el = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, w.full_block_table, 1.0)
+    assert_close(f"verify O (B={B}, q_len={q_len}, splits={ns})", o.cpu().numpy(), eo, O_TOL)
+    assert_close(f"verify LSE (B={B}, q_len={q_len}, splits={ns})", lse.cpu().numpy(), el, LSE_TOL)
+
+
 def test_window_longer_than_sequence_gives_empty_rows():
     w, pool = workload(2, batch=2, seq_len=100, n_decode=1, n_verify=1)
     w.seq_lens[:] = [3, 100]
