@@ -69,6 +69,35 @@ def test_scheduled_equals_balanced(config, kw):
         assert torch.equal(l1, l2), f"lse differs at step {s}"
 
 
+@pytest.mark.parametrize("seed", range(16))
+def test_random_batches_scheduled_equals_balanced(seed):
+    # seeded random batches: 1-70 sequences (the map reads lengths 64 at a
+    # time), lengths 1-4096, per-sequence budgets, bf16 or fp8, page- or
+    # token-granular views; the scheduled call must equal the balanced one
+    rng = np.random.default_rng(777 + seed)
+    cfg = 2 if seed % 2 == 0 else 5
+    B = int(rng.choice([1, 3, 8, 33, 64, 65, 70]))
+    w = make_workload(cfg, device="cuda", batch=B, seq_len=4096 if cfg == 2 else 5000,
+                      n_decode=2, n_verify=1, with_kv=True)
+    w.seq_lens[:] = rng.integers(1, 4097, B).astype(np.int32)
+    budget = np.array([int(rng.integers(0, int(L) + 1)) for L in w.seq_lens], dtype=np.int32)
+    token = seed % 3 == 0
+    cap = w.max_pages_per_seq
+    plan = K.compile_plan(
+        dev_i32(w.seq_lens), dev_i32(w.full_block_table), dev_i32(w.span_offsets),
+        dev_i32(w.span_start), dev_i32(w.span_len),
+        torch.as_tensor(np.asarray(w.span_prior, dtype=np.float32)).cuda(), dev_i32(w.prefix),
+        dev_i32(w.suffix), dev_i32(budget), num_pages=w.num_pages, view_capacity=cap,
+        token_granular=token)
+    torch.cuda.synchronize()
+    mask = plan["view_token_mask"] if token else None
+    sched, got = _pair(w, plan, cap, mask, range(2))
+    assert sched.numel() > 0
+    for s, ((o1, l1), (o2, l2)) in enumerate(got):
+        assert torch.equal(o1, o2), f"out differs at step {s} (B={B}, token={token})"
+        assert torch.equal(l1, l2), f"lse differs at step {s} (B={B}, token={token})"
+
+
 def test_scheduled_token_granular_view():
     w = make_workload(4, device="cuda", n_decode=2, n_verify=1)
     plan, cap, mask = _view(w, token_granular=True)
