@@ -24,6 +24,9 @@
 // hi = P truncated to bf16, lo = P - hi (exact in fp32) truncated to bf16,
 // which keeps the probability rounding error below 2^-14 relative.
 // The causal mask and the partial last page are handled on the last pages only.
+// When the last row tile holds a single window token (q_len = 4 t + 1), its
+// softmax runs on that token's 4 rows gathered into all 64 lanes rather than
+// on 16 rows of which 12 are padding (the C4 kernel instances).
 // The four wavefronts combine through LDS; with several splits, the workgroup
 // that finishes last for its (sequence, KV head) merges all splits (atomic
 // arrival counter in the workspace), so one launch produces the final output.
