@@ -62,6 +62,25 @@ __device__ __forceinline__ uint32_t range_bits(int w, int x, int e) {
   return (uint32_t)(((1ull << hi) - 1ull) ^ ((1ull << lo) - 1ull));
 }
 
+// Number of clear bits of the bitmap in [x, e), x < e. The words are read kW
+// at a time before they are counted, so that their LDS latencies overlap: a
+// span covers tens of words in the token bitmap, one to three in the page
+// bitmap. Reads past the last word repeat it and count nothing, as range_bits
+// is zero there.
+template <int kW>
+__device__ __forceinline__ int count_clear(const uint32_t* bitmap, int x, int e) {
+  const int w1 = (e - 1) >> 5;
+  int c = 0;
+  for (int w = x >> 5; w <= w1; w += kW) {
+    uint32_t b[kW];
+#pragma unroll
+    for (int k = 0; k < kW; ++k) b[k] = bitmap[min(w + k, w1)];
+#pragma unroll
+    for (int k = 0; k < kW; ++k) c += __popc(range_bits(w + k, x, e) & ~b[k]);
+  }
+  return c;
+}
+
 template <bool TOK>
 __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) {
   extern __shared__ uint32_t bitmap[];   // page mode: bit per page; token mode: bit per token
@@ -308,10 +327,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
       const bool valid = e > x;                         // empty spans are ignored
       const int u0 = TOK ? x : x / kPage;
       const int u1 = TOK ? e : (e + kPage - 1) / kPage;
-      int fresh = 0;
-      if (valid)
-        for (int w = u0 >> 5; w <= (u1 - 1) >> 5; ++w)
-          fresh += __popc(range_bits(w, u0, u1) & ~bitmap[w]);
+      int fresh = valid ? count_clear<TOK ? 4 : 1>(bitmap, u0, u1) : 0;
       bool my_taken = false;
       int pos = 0;                                      // lanes below pos are decided
       while (true) {
@@ -335,11 +351,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
         my_taken |= lane == j;
         pos = j + 1;
         const int c0 = max(u0, ju0), c1 = min(u1, ju1);
-        int delta = 0;
-        if (valid && lane > j && c0 < c1)
-          for (int w = c0 >> 5; w <= (c1 - 1) >> 5; ++w)
-            delta += __popc(range_bits(w, c0, c1) & ~bitmap[w]);
-        fresh -= delta;
+        if (valid && lane > j && c0 < c1) fresh -= count_clear<TOK ? 4 : 1>(bitmap, c0, c1);
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
         const int jw0 = ju0 >> 5, jw1 = (ju1 - 1) >> 5;
         for (int wb = jw0; wb <= jw1; wb += 64) {
