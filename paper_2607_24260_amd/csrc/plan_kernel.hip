@@ -62,23 +62,41 @@ __device__ __forceinline__ uint32_t range_bits(int w, int x, int e) {
   return (uint32_t)(((1ull << hi) - 1ull) ^ ((1ull << lo) - 1ull));
 }
 
-// Number of clear bits of the bitmap in [x, e), x < e. The words are read kW
-// at a time before they are counted, so that their LDS latencies overlap: a
-// span covers tens of words in the token bitmap, one to three in the page
-// bitmap. Reads past the last word repeat it and count nothing, as range_bits
-// is zero there.
-template <int kW>
+// Spare words past the last bitmap word: count_clear reads up to 7 of them.
+constexpr int kBitmapPadWords = 8;
+
+// Number of clear bits of the bitmap in [x, e), x < e.
+// Page bitmap: a span covers one to three words, counted one at a time.
+// Token bitmap: a span covers tens of words. The count is the length of the
+// range less its set bits, which are summed over the whole words w0 .. w1 (a
+// popcount with accumulate per word) and corrected by the set bits of the two
+// end words that lie outside [x, e). The words are read eight at a time before
+// they are counted, so that their LDS latencies overlap; a batch may read up
+// to seven words past w1 (into the spare words at the end) and counts nothing
+// there.
+template <bool TOK>
 __device__ __forceinline__ int count_clear(const uint32_t* bitmap, int x, int e) {
-  const int w1 = (e - 1) >> 5;
-  int c = 0;
-  for (int w = x >> 5; w <= w1; w += kW) {
-    uint32_t b[kW];
+  if constexpr (!TOK) {
+    int c = 0;
+    for (int w = x >> 5; w <= (e - 1) >> 5; ++w) c += __popc(range_bits(w, x, e) & ~bitmap[w]);
+    return c;
+  } else {
+    constexpr int kW = 8;
+    static_assert(kW <= kBitmapPadWords, "batch reads past the spare words");
+    const int w0 = x >> 5, w1 = (e - 1) >> 5;
+    const uint32_t below = (1u << (x & 31)) - 1u;            // bits of w0 before x
+    const uint32_t above = ~((2u << ((e - 1) & 31)) - 1u);   // bits of w1 from e on
+    int set = -(int)(__popc(bitmap[w0] & below) + __popc(bitmap[w1] & above));
+    for (int w = w0; w <= w1; w += kW) {
+      uint32_t v[kW];
 #pragma unroll
-    for (int k = 0; k < kW; ++k) b[k] = bitmap[min(w + k, w1)];
+      for (int k = 0; k < kW; ++k) v[k] = bitmap[w + k];
+      const int last = w1 - w;
 #pragma unroll
-    for (int k = 0; k < kW; ++k) c += __popc(range_bits(w + k, x, e) & ~b[k]);
+      for (int k = 0; k < kW; ++k) set += __popc(k <= last ? v[k] : 0u);
+    }
+    return (e - x) - set;
   }
-  return c;
 }
 
 template <bool TOK>
@@ -327,7 +345,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
       const bool valid = e > x;                         // empty spans are ignored
       const int u0 = TOK ? x : x / kPage;
       const int u1 = TOK ? e : (e + kPage - 1) / kPage;
-      int fresh = valid ? count_clear<TOK ? 4 : 1>(bitmap, u0, u1) : 0;
+      int fresh = valid ? count_clear<TOK>(bitmap, u0, u1) : 0;
       bool my_taken = false;
       int pos = 0;                                      // lanes below pos are decided
       while (true) {
@@ -351,7 +369,7 @@ __global__ __launch_bounds__(kPlanThreads) void compile_plan_kernel(PlanArgs a) 
         my_taken |= lane == j;
         pos = j + 1;
         const int c0 = max(u0, ju0), c1 = min(u1, ju1);
-        if (valid && lane > j && c0 < c1) fresh -= count_clear<TOK ? 4 : 1>(bitmap, c0, c1);
+        if (valid && lane > j && c0 < c1) fresh -= count_clear<TOK>(bitmap, c0, c1);
         __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
         const int jw0 = ju0 >> 5, jw1 = (ju1 - 1) >> 5;
         for (int wb = jw0; wb <= jw1; wb += 64) {
@@ -455,7 +473,7 @@ size_t plan_lds_bytes(int fbt_stride, bool token_mode) {
   // page mode: a bit per page; token mode: a bit per token (16 per page)
   const size_t words = token_mode ? ((size_t)fbt_stride * kPage + 31) / 32
                                   : ((size_t)fbt_stride + 31) / 32;
-  return (words + 1) * sizeof(uint32_t);   // + a spare word
+  return (words + kBitmapPadWords) * sizeof(uint32_t);
 }
 
 }  // namespace
