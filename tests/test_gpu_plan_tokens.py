@@ -128,6 +128,30 @@ def test_largest_supported_stride():
     run_both([L], [np.arange(16384)], [spans], [1000], [300], [60000])
 
 
+@pytest.mark.parametrize("L", [16384 * 16, 16384 * 16 - 5])
+@pytest.mark.parametrize("policy", [0, 1])
+def test_spans_reaching_the_last_bitmap_word(L, policy):
+    # Spans that end at L or are clipped there, single-token spans and spans
+    # on word boundaries in the last words of the largest token bitmap: a
+    # span's price counts the clear bits of its range eight words at a time
+    # past its last word, and the end words by their bits inside the range.
+    # With the mandatory last token, the hand-picked spans cost 39, 0, 255,
+    # 0, 0, 33 and 160 tokens in rank order (488 in all), so a budget one
+    # below that total rejects exactly the last of them.
+    hand = [(L - 40, 40, 0.99), (L - 3, 10, 0.98), (L - 32 * 9 - 7, 300, 0.97),
+            (L - 1, 1, 0.96), (L - 64, 1, 0.95), (L - 700, 33, 0.94),
+            (L - 32 * 20, 32 * 5, 0.93)]
+    rng = np.random.default_rng(11)
+    rand = [(int(rng.integers(L - 3000, L)), int(rng.integers(1, 600)), float(rng.random()) * 0.9)
+            for _ in range(60)]
+    fbt = [np.arange(16384)]
+    for budget in (488, 487, 489):
+        gpu, plans = run_both([L], fbt, [hand], [0], [1], [budget], policy=policy)
+        assert plans[0].view_tokens == (488 if budget >= 488 else 328)
+    for budget in (100, 400, 1200, 2500):
+        run_both([L], fbt, [hand + rand], [0], [1], [budget], policy=policy)
+
+
 @pytest.mark.parametrize("config", [2, 4])
 def test_workload_plans(config):
     w = make_workload(config, device="cuda", n_decode=1, n_verify=1, with_kv=False)
