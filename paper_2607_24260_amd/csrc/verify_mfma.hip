@@ -78,6 +78,10 @@ __device__ __forceinline__ float dpp_into(float old, float src) {
   return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(src), CTRL,
                                                     0xF, BANKS, false));
 }
+template <int CTRL, int BANKS>
+__device__ __forceinline__ uint32_t dpp_into(uint32_t old, uint32_t src) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)src, CTRL, 0xF, BANKS, false);
+}
 // x moved by CTRL in every lane; a lane whose source lies outside its row reads 0
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_all(uint32_t x) {
@@ -450,10 +454,14 @@ void verify_mfma_kernel(AttnArgs a) {
           const float pl0 = pv0 - __uint_as_float(__float_as_uint(pv0) & 0xffff0000u);
           const float pl1 = pv1 - __uint_as_float(__float_as_uint(pv1) & 0xffff0000u);
           const uint32_t h = pack_bf16_exact(pv0, pv1), lw = pack_bf16_exact(pl0, pl1);
-          // back to lane (j, n): the pieces of lanes 16 j + 4 c + n, c = 0..3
-          phi[nt] = u32x4{h, dpp_all<kRowShl(4)>(h), dpp_all<kRowShl(8)>(h), dpp_all<kRowShl(12)>(h)};
-          plo[nt] = u32x4{lw, dpp_all<kRowShl(4)>(lw), dpp_all<kRowShl(8)>(lw),
-                          dpp_all<kRowShl(12)>(lw)};
+          // Back to the P^T operand, with the hi and lo weights side by side
+          // so that one product per V tile takes both: column n < 4 (lane
+          // (j, n)) gets row n's hi pieces, from lanes 16 j + 4 c + n, c = 0..3;
+          // column 4 + n gets row n's lo pieces from the same lanes. The two
+          // column groups are added when the wavefronts combine.
+          phi[nt] = u32x4{dpp_into<kRowShr(4), 0x2>(h, lw), dpp_into<kRowShl(4), 0x1>(lw, h),
+                          dpp_into<kRowShl(4), 0x2>(dpp_all<kRowShl(8)>(h), lw),
+                          dpp_into<kRowShl(8), 0x2>(dpp_all<kRowShl(12)>(h), lw)};
           continue;
         }
       }
@@ -517,7 +525,7 @@ void verify_mfma_kernel(AttnArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         acc[nt][dt] = mfma(vop, phi[nt], acc[nt][dt]);
-        acc[nt][dt] = mfma(vop, plo[nt], acc[nt][dt]);
+        if (!(C4 && nt == NT - 1)) acc[nt][dt] = mfma(vop, plo[nt], acc[nt][dt]);
       }
     }
     if constexpr (KV == kBF16) next_v();
@@ -585,6 +593,12 @@ void verify_mfma_kernel(AttnArgs a) {
     }
     lt = xor16_sum(lt);
     lt = xor32_sum(lt);
+    if (C4 && nt == NT - 1) {   // the gathered tile: row n's lo part sits in column 4 + n
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[nt][dt][e] += dpp_all<kRowShl(4)>(acc[nt][dt][e]);
+    }
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt)
       *reinterpret_cast<f32x4 *>(&s_acc[wave][n][dt * 16 + 4 * j]) = acc[nt][dt];
