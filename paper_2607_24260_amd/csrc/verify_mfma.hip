@@ -26,7 +26,8 @@
 // The causal mask and the partial last page are handled on the last pages only.
 // When the last row tile holds a single window token (q_len = 4 t + 1), its
 // softmax runs on that token's 4 rows gathered into all 64 lanes rather than
-// on 16 rows of which 12 are padding (the C4 kernel instances).
+// on 16 rows of which 12 are padding, and its hi and lo weights share one PV
+// product (columns 0-3 and 4-7 of the operand) (the C4 kernel instances).
 // The four wavefronts combine through LDS; with several splits, the workgroup
 // that finishes last for its (sequence, KV head) merges all splits (atomic
 // arrival counter in the workspace), so one launch produces the final output.
