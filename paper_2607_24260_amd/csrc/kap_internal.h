@@ -518,6 +518,26 @@ __device__ __forceinline__ bool last_arrival(const AttnArgs &a, int b, int g, in
   return *flag != 0;
 }
 
+// last_arrival for a workgroup whose wavefronts may all have written part of
+// its partial: each waits until its own stores are complete, the workgroup
+// meets at a barrier, and one thread takes the ticket.
+__device__ __forceinline__ bool last_arrival_all(const AttnArgs &a, int b, int g, int n_split,
+                                                 int *flag) {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's stores are complete
+  asm volatile("" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int32_t *ctr = a.tickets + ((size_t)b * a.Hkv + g) * kTicketStride;
+    const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = (prev == n_split - 1) ? 1 : 0;
+    if (last) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last;
+  }
+  __syncthreads();
+  return *flag != 0;
+}
+
 // LSE merge of the ns partials (slots slot0 .. slot0 + ns - 1) of the R_loc
 // local rows of (b, g), D = 128:
 // lse = log2 sum_s 2^lse_s, o = sum_s 2^(lse_s - lse) o_s (empty splits drop out).

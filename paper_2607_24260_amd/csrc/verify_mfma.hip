@@ -251,9 +251,15 @@ void verify_mfma_kernel(AttnArgs a) {
   __shared__ float s_acc[kVerifyWaves][16][kD + 4];
   __shared__ float s_m[kVerifyWaves][16];
   __shared__ float s_l[kVerifyWaves][16];
-  __shared__ float s_out[16][kD];
-  __shared__ float s_olse[16];
   __shared__ int s_flag;
+  // Where the combined tiles go: every thread stores its own slice, except in
+  // the three-tile fp8 kernel for 10-12-token windows, which stages each tile
+  // in LDS for wavefront 0 to store -- at 256 registers there, storing from
+  // every thread moved spills into its page loop (ragged fp8 11-token windows
+  // 957 vs 1250 us on MI355X).
+  constexpr bool kStagedStore = KV == kFP8 && NT == 3 && !C4;
+  __shared__ float s_out[kStagedStore ? 16 : 1][kD];
+  __shared__ float s_olse[16];
 
   WorkItem wi;
   int L;
@@ -608,16 +614,18 @@ void verify_mfma_kernel(AttnArgs a) {
       s_l[wave][n] = lt;
     }
     __syncthreads();
+    // thread (rn, d8) combines row rn's dims d8 .. d8 + 7
     const int rn = threadIdx.x >> 4;            // row of the tile
     const int d8 = (threadIdx.x & 15) * 8;      // 8 dims
-    {
+    const int r = nt * 16 + rn;
+    float o[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = 0.f;
+    float lse2 = -INFINITY;
+    if (r < R) {
       float M = -INFINITY;
 #pragma unroll
       for (int w = 0; w < kVerifyWaves; ++w) M = fmaxf(M, s_m[w][rn]);
-      float o[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = 0.f;
-      float lse2 = -INFINITY;
       if (M != -INFINITY) {
         float den = 0.f;
 #pragma unroll
@@ -632,41 +640,64 @@ void verify_mfma_kernel(AttnArgs a) {
         for (int e = 0; e < 8; ++e) o[e] *= inv;
         lse2 = M + log2f(den);
       }
-      *reinterpret_cast<float4 *>(&s_out[rn][d8]) = make_float4(o[0], o[1], o[2], o[3]);
-      *reinterpret_cast<float4 *>(&s_out[rn][d8 + 4]) = make_float4(o[4], o[5], o[6], o[7]);
-      if (d8 == 0) s_olse[rn] = lse2;
     }
-    __syncthreads();
-    // wavefront 0 writes the tile (final output, or this split's partial)
-    if (threadIdx.x < 64) {
-      const auto ro = partial_rsrc(a.part_o);
-      const auto rl = partial_rsrc(a.part_lse);
+    const float4 v0 = make_float4(o[0], o[1], o[2], o[3]);
+    const float4 v1 = make_float4(o[4], o[5], o[6], o[7]);
+    if constexpr (kStagedStore) {
+      // staged in LDS; wavefront 0 writes the tile
+      *reinterpret_cast<float4 *>(&s_out[rn][d8]) = v0;
+      *reinterpret_cast<float4 *>(&s_out[rn][d8 + 4]) = v1;
+      if (d8 == 0) s_olse[rn] = lse2;
+      __syncthreads();
+      if (threadIdx.x < 64) {
+        const auto ro = partial_rsrc(a.part_o);
+        const auto rl = partial_rsrc(a.part_lse);
 #pragma unroll
-      for (int t8 = 0; t8 < 8; ++t8) {
-        const int f = threadIdx.x + 64 * t8;      // float4 index in [16][128]
-        const int rr = f >> 5, d4 = (f & 31) * 4;
-        const int r = nt * 16 + rr;
-        if (r < R) {
-          const size_t row = out_row(a, b, g, r);
-          const float4 v = *reinterpret_cast<const float4 *>(&s_out[rr][d4]);
-          if (n_split == 1)
-            *reinterpret_cast<float4 *>(a.out + row * kD + d4) = v;
-          else
-            partial_store4(ro, (((size_t)(wi.slot0 + split) * R + r) * kD + d4) * 4, v);
+        for (int t8 = 0; t8 < 8; ++t8) {
+          const int f = threadIdx.x + 64 * t8;      // float4 index in [16][128]
+          const int rr = f >> 5, d4 = (f & 31) * 4;
+          const int rw = nt * 16 + rr;
+          if (rw < R) {
+            const size_t row = out_row(a, b, g, rw);
+            const float4 v = *reinterpret_cast<const float4 *>(&s_out[rr][d4]);
+            if (n_split == 1)
+              *reinterpret_cast<float4 *>(a.out + row * kD + d4) = v;
+            else
+              partial_store4(ro, (((size_t)(wi.slot0 + split) * R + rw) * kD + d4) * 4, v);
+          }
+        }
+        if (threadIdx.x < 16 && nt * 16 + threadIdx.x < R) {
+          const size_t row = out_row(a, b, g, nt * 16 + threadIdx.x);
+          if (n_split == 1) a.lse[row] = s_olse[threadIdx.x] * kLn2;
+          else partial_store1(rl, ((size_t)(wi.slot0 + split) * R + nt * 16 + threadIdx.x) * 4,
+                              s_olse[threadIdx.x]);
         }
       }
-      if (threadIdx.x < 16 && nt * 16 + threadIdx.x < R) {
-        const size_t row = out_row(a, b, g, nt * 16 + threadIdx.x);
-        if (n_split == 1) a.lse[row] = s_olse[threadIdx.x] * kLn2;
-        else partial_store1(rl, ((size_t)(wi.slot0 + split) * R + nt * 16 + threadIdx.x) * 4,
-                            s_olse[threadIdx.x]);
+      __syncthreads();
+    } else {
+      // each thread writes its slice: the final output, or its part of this
+      // split's partial
+      if (r < R) {
+        if (n_split == 1) {
+          const size_t row = out_row(a, b, g, r);
+          *reinterpret_cast<float4 *>(a.out + row * kD + d8) = v0;
+          *reinterpret_cast<float4 *>(a.out + row * kD + d8 + 4) = v1;
+          if (d8 == 0) a.lse[row] = lse2 * kLn2;
+        } else {
+          const size_t pr = (size_t)(wi.slot0 + split) * R + r;
+          const auto ro = partial_rsrc(a.part_o);
+          partial_store4(ro, (pr * kD + d8) * 4, v0);
+          partial_store4(ro, (pr * kD + d8 + 4) * 4, v1);
+          if (d8 == 0) partial_store1(partial_rsrc(a.part_lse), pr * 4, lse2);
+        }
       }
+      if (nt + 1 < NT) __syncthreads();   // the next tile reuses s_acc, s_m, s_l
     }
-    __syncthreads();
   }
 
   // ---- the last workgroup of (b, g) merges the splits ---------------------------------
-  if (n_split > 1 && last_arrival(a, b, g, n_split, &s_flag))
+  if (n_split > 1 && (kStagedStore ? last_arrival(a, b, g, n_split, &s_flag)
+                                    : last_arrival_all(a, b, g, n_split, &s_flag)))
     merge_rows<3>(a, b, g, R, wi.slot0, n_split);
 }
 
