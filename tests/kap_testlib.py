@@ -100,7 +100,8 @@ def assert_close(name, got, want, tol, mask=None):
     if mask is not None:
         got, want = got[mask], want[mask]
     both_inf = np.isinf(got) & np.isinf(want) & (np.sign(got) == np.sign(want))
-    diff = np.where(both_inf, 0.0, np.abs(got - want))
+    with np.errstate(invalid="ignore"):          # inf - inf where both_inf masks it
+        diff = np.where(both_inf, 0.0, np.abs(got - want))
     worst = float(np.nanmax(diff)) if diff.size else 0.0
     assert not np.isnan(diff).any(), f"{name}: NaN"
     assert worst <= tol, f"{name}: max abs err {worst:.3e} > {tol:.1e}"

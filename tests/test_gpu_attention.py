@@ -232,6 +232,26 @@ def test_split_merge_of_long_windows(kv_dtype):
         w.q_verify = orig
 
 
+@pytest.mark.parametrize("kv_dtype,q_len", [("bf16", 5), ("bf16", 11), ("fp8", 5), ("fp8", 9),
+                                             ("fp8", 11), ("fp8", 12), ("fp8", 13)])
+def test_combined_tile_stores_at_every_split_count(kv_dtype, q_len):
+    # After the wavefronts combine, a verify workgroup writes each row tile
+    # either from every thread or staged through LDS by one wavefront (the
+    # kernel instance decides), as the final output (one split) or as its
+    # split's partial for the merge: each way at 1, 3 and the maximum number
+    # of splits, on ragged lengths with a sequence shorter than the window.
+    cfg = 2 if kv_dtype == "bf16" else 5
+    w, pool = _ragged(cfg, 3, 4096 if cfg == 2 else 5000, [2500, 777, q_len - 1])
+    q = _window(w, q_len, 700 + q_len)
+    for ns in (1, 3, 10_000):
+        o, lse = K.verify(kv_of(w), q, dev_i32(w.seq_lens), dev_i32(w.full_block_table),
+                          2500, 1.0, num_splits=ns)
+        torch.cuda.synchronize()
+        eo, el = O.verify(pool, q.float().cpu().numpy(), w.seq_lens, w.full_block_table, 1.0)
+        assert_close(f"verify O (q_len={q_len}, splits={ns})", o.cpu().numpy(), eo, O_TOL)
+        assert_close(f"verify LSE (q_len={q_len}, splits={ns})", lse.cpu().numpy(), el, LSE_TOL)
+
+
 def test_view_order_does_not_matter():
     w, pool = workload(2, batch=2, seq_len=4000, n_decode=1, n_verify=1)
     plan = gpu_plan(w)
