@@ -191,3 +191,24 @@ def test_long_overlapping_spans_many_taken(policy, frac):
                         [int(frac * L)], policy=policy)
     if frac == 1.0 and policy == 0:
         assert plans[0].spans_taken == sum(1 for s, n, _ in spans if min(L, s + n) > max(0, s))
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_largest_supported_stride(policy):
+    # fbt_stride = 262144 pages (4194304 tokens, a 32 KB page bitmap), one
+    # full-length sequence under a permuted table: spans that end at L, are
+    # clipped there or sit in the last bitmap words, and budgets whose views
+    # stay within the 2048 pages staged in LDS before the table is read and
+    # go past them (each page then mapped where it is found)
+    rng = np.random.default_rng(9 + policy)
+    stride = 262144
+    L = stride * 16
+    spans = [(int(rng.integers(0, L)), int(rng.integers(1, 20000)), float(rng.random()) * 0.9)
+             for _ in range(300)]
+    spans += [(L - 40, 40, 0.99), (L - 3, 10, 0.98), (L - 16 * 32 * 3 - 7, 5000, 0.97),
+              (L - 1, 1, 0.96), (L - 16 * 70, 16 * 33, 0.95), (0, 16 * 5000, 0.5)]
+    fbt = [rng.permutation(stride)]
+    for budget in (20000, 400000, 2000000):
+        _, plans = run_both([L], fbt, [spans], [1000], [300], [budget], policy=policy)
+        assert plans[0].status == O.PLAN_OK
+    assert plans[0].num_blocks > 2048
